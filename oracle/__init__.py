@@ -1,0 +1,205 @@
+"""CPU fp64 oracle for the differentiable Adam step and tree pack/unpack.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the smoke check and by
+the CPU-baseline leg of the benchmark, never by the product path.  It shares
+no code with the HIP library.  The arithmetic lives in ``oracle.c`` (plain C,
+fp64, single thread, no FMA contraction); this module only marshals numpy
+arrays into it.  The header of ``oracle.c`` lists the paper passages each
+function follows, the readings taken where the paper is silent, and the pins
+that tie each function to something other than itself.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+# Plain C, no fast-math, no contraction: every operation is one IEEE double op.
+CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math"]
+
+
+def build(force: bool = False) -> str:
+    """Compile oracle.c into liboracle.so next to it (gcc)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB)
+        d = ctypes.POINTER(ctypes.c_double)
+        i64 = ctypes.c_int64
+        f64 = ctypes.c_double
+        hyper = [i64, f64, f64, f64, f64, f64]  # count, lr, b1, b2, eps, eps_root
+        lib.oracle_adam_fwd.argtypes = [i64, d, d, d, d, *hyper, d, d, d, d]
+        lib.oracle_adam_bwd.argtypes = [i64, d, d, d, d, d, d, *hyper, d, d, d, d]
+        lib.oracle_adam_fwd_mag.argtypes = [i64, d, d, d, d, *hyper, d, d, d, d]
+        lib.oracle_adam_bwd_mag.argtypes = [i64, d, d, d, d, d, d, *hyper, d, d, d]
+        lib.oracle_unrolled_fwd.argtypes = [i64, i64, d, d, d, d, *hyper, d, d, d]
+        lib.oracle_unrolled_bwd.argtypes = [i64, i64, d, d, d, d, *hyper, d, d, d, d]
+        vp = ctypes.c_void_p
+        lib.oracle_pack.argtypes = [i64, ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
+                                    ctypes.POINTER(vp), vp]
+        lib.oracle_unpack.argtypes = [i64, ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
+                                      vp, ctypes.POINTER(vp)]
+        for f in ("oracle_adam_fwd", "oracle_adam_bwd", "oracle_adam_fwd_mag",
+                  "oracle_adam_bwd_mag", "oracle_unrolled_fwd", "oracle_unrolled_bwd",
+                  "oracle_pack", "oracle_unpack"):
+            getattr(lib, f).restype = None
+        _lib = lib
+    return _lib
+
+
+def _f64(x, n=None):
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.float64).reshape(-1))
+    if n is not None and a.size != n:
+        raise ValueError("expected %d elements, got %d" % (n, a.size))
+    return a
+
+
+def _ptr(a):
+    if a is None:
+        return None
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _hyper(count, lr, b1, b2, eps, eps_root):
+    return [int(count), float(lr), float(b1), float(b2), float(eps), float(eps_root)]
+
+
+def adam_fwd(p, g, m, v, count, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, eps_root=0.0):
+    """One Adam step; returns (p', m', v', u) as fp64 arrays."""
+    p = _f64(p)
+    n = p.size
+    g, m, v = _f64(g, n), _f64(m, n), _f64(v, n)
+    outs = [np.empty(n) for _ in range(4)]
+    _load().oracle_adam_fwd(n, _ptr(p), _ptr(g), _ptr(m), _ptr(v),
+                            *_hyper(count, lr, b1, b2, eps, eps_root), *map(_ptr, outs))
+    return tuple(outs)
+
+
+def adam_bwd(dP, dM, dV, g, m, v, count, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, eps_root=0.0):
+    """VJP of one Adam step; dM/dV may be None (zero).  Returns (dp, dg, dm, dv)."""
+    dP = _f64(dP)
+    n = dP.size
+    dM = None if dM is None else _f64(dM, n)
+    dV = None if dV is None else _f64(dV, n)
+    g, m, v = _f64(g, n), _f64(m, n), _f64(v, n)
+    outs = [np.empty(n) for _ in range(4)]
+    _load().oracle_adam_bwd(n, _ptr(dP), _ptr(dM), _ptr(dV), _ptr(g), _ptr(m), _ptr(v),
+                            *_hyper(count, lr, b1, b2, eps, eps_root), *map(_ptr, outs))
+    return tuple(outs)
+
+
+def adam_fwd_mag(p, g, m, v, count, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, eps_root=0.0):
+    """Tolerance scales (mag_p, mag_m, mag_v, mag_u) of the forward outputs."""
+    p = _f64(p)
+    n = p.size
+    g, m, v = _f64(g, n), _f64(m, n), _f64(v, n)
+    outs = [np.empty(n) for _ in range(4)]
+    _load().oracle_adam_fwd_mag(n, _ptr(p), _ptr(g), _ptr(m), _ptr(v),
+                                *_hyper(count, lr, b1, b2, eps, eps_root), *map(_ptr, outs))
+    return tuple(outs)
+
+
+def adam_bwd_mag(dP, dM, dV, g, m, v, count, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8,
+                 eps_root=0.0):
+    """Tolerance scales (mag_dg, mag_dm, mag_dv) of the backward outputs."""
+    dP = _f64(dP)
+    n = dP.size
+    dM = None if dM is None else _f64(dM, n)
+    dV = None if dV is None else _f64(dV, n)
+    g, m, v = _f64(g, n), _f64(m, n), _f64(v, n)
+    outs = [np.empty(n) for _ in range(3)]
+    _load().oracle_adam_bwd_mag(n, _ptr(dP), _ptr(dM), _ptr(dV), _ptr(g), _ptr(m), _ptr(v),
+                                *_hyper(count, lr, b1, b2, eps, eps_root), *map(_ptr, outs))
+    return tuple(outs)
+
+
+def unrolled_fwd(p0, grads, m0, v0, count0, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8,
+                 eps_root=0.0):
+    """K steps from (p0, m0, v0) with grads [K, n].  Returns (pK, m_traj, v_traj),
+    the trajectories shaped [K+1, n] with entry 0 equal to m0 / v0."""
+    p0 = _f64(p0)
+    n = p0.size
+    grads = np.ascontiguousarray(np.asarray(grads, dtype=np.float64).reshape(-1, n))
+    K = grads.shape[0]
+    m0, v0 = _f64(m0, n), _f64(v0, n)
+    pK = np.empty(n)
+    mt = np.empty((K + 1, n))
+    vt = np.empty((K + 1, n))
+    _load().oracle_unrolled_fwd(K, n, _ptr(p0), _ptr(grads), _ptr(m0), _ptr(v0),
+                                *_hyper(count0, lr, b1, b2, eps, eps_root),
+                                _ptr(pK), _ptr(mt), _ptr(vt))
+    return pK, mt, vt
+
+
+def unrolled_bwd(dpK, grads, m_traj, v_traj, count0, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8,
+                 eps_root=0.0):
+    """Reverse pass through K steps.  Returns (dp0, dg [K, n], dm0, dv0)."""
+    dpK = _f64(dpK)
+    n = dpK.size
+    grads = np.ascontiguousarray(np.asarray(grads, dtype=np.float64).reshape(-1, n))
+    K = grads.shape[0]
+    mt = np.ascontiguousarray(np.asarray(m_traj, dtype=np.float64).reshape(K + 1, n))
+    vt = np.ascontiguousarray(np.asarray(v_traj, dtype=np.float64).reshape(K + 1, n))
+    dp0, dm0, dv0 = np.empty(n), np.empty(n), np.empty(n)
+    dg = np.empty((K, n))
+    _load().oracle_unrolled_bwd(K, n, _ptr(dpK), _ptr(grads), _ptr(mt), _ptr(vt),
+                                *_hyper(count0, lr, b1, b2, eps, eps_root),
+                                _ptr(dp0), _ptr(dg), _ptr(dm0), _ptr(dv0))
+    return dp0, dg, dm0, dv0
+
+
+def _seg_args(numel, offsets):
+    numel = np.ascontiguousarray(np.asarray(numel, dtype=np.int64).reshape(-1))
+    offs = None if offsets is None else np.ascontiguousarray(
+        np.asarray(offsets, dtype=np.int64).reshape(-1))
+    p64 = ctypes.POINTER(ctypes.c_int64)
+    return numel, offs, numel.ctypes.data_as(p64), (None if offs is None else offs.ctypes.data_as(p64))
+
+
+def pack(leaves, flat_len=None, offsets=None, dtype=None):
+    """Pack a list of numpy arrays (same dtype) into a new flat array by byte copy.
+    Gaps (explicit offsets) are left zero."""
+    leaves = [np.ascontiguousarray(x) for x in leaves]
+    if dtype is None:
+        dtype = leaves[0].dtype if leaves else np.float32
+    dtype = np.dtype(dtype)
+    numel = [x.size for x in leaves]
+    for x in leaves:
+        if x.dtype.itemsize != dtype.itemsize:
+            raise ValueError("all leaves must share the element size")
+    if flat_len is None:
+        flat_len = (sum(numel) if offsets is None else
+                    max([o + k for o, k in zip(offsets, numel)] + [0]))
+    flat = np.zeros(flat_len, dtype=dtype)
+    numel_a, offs_a, pn, po = _seg_args(numel, offsets)
+    ptrs = (ctypes.c_void_p * max(len(leaves), 1))(*[x.ctypes.data for x in leaves])
+    _load().oracle_pack(len(leaves), pn, po, dtype.itemsize, ptrs, flat.ctypes.data)
+    return flat
+
+
+def unpack(flat, shapes, offsets=None):
+    """Split a flat numpy array into new arrays of the given shapes by byte copy."""
+    flat = np.ascontiguousarray(flat)
+    leaves = [np.empty(s, dtype=flat.dtype) for s in shapes]
+    numel = [x.size for x in leaves]
+    numel_a, offs_a, pn, po = _seg_args(numel, offsets)
+    ptrs = (ctypes.c_void_p * max(len(leaves), 1))(*[x.ctypes.data for x in leaves])
+    _load().oracle_unpack(len(leaves), pn, po, flat.dtype.itemsize, flat.ctypes.data, ptrs)
+    return leaves

@@ -1,0 +1,294 @@
+/*
+ * oracle.c -- plain CPU reference for the differentiable Adam step, its
+ * vector-Jacobian product, the K-step unrolled driver and tree pack/unpack.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the checker the GPU path is judged
+ * against.  Only the test-suite, the smoke check and the CPU-baseline leg of
+ * the benchmark may load it.  It shares no source, header, table or helper
+ * with the HIP library, and the HIP library never calls it.
+ *
+ * Conventions:
+ *   - fp64 everywhere; callers upcast fp32 inputs element by element (exact).
+ *   - single thread, scalar loops, no blocking, no fusion beyond the
+ *     definition; built with -O2 -ffp-contract=off and without -ffast-math,
+ *     so every operation is a separately rounded IEEE double operation.
+ *
+ * What the paper fixes and what it does not (TorchOpt, arXiv 2211.06934):
+ *   - Sec. 2.3 "CPU/GPU-accelerated optimizers": Adam is treated as ONE
+ *     differentiable operator with a hand-written forward and backward, and
+ *     some 0/0 cases are cancelled explicitly.  The paper prints no Adam
+ *     formula.  The forward below is Adam as defined by Kingma & Ba (ICLR
+ *     2015, Algorithm 1), with an extra eps_root term inside the square root
+ *     (eps_root = 0 gives the textbook update).
+ *   - Listing 1 (explicit gradient, functional API): a non-inplace update
+ *     followed by apply_updates, repeated for iter_times steps, then one
+ *     backward pass through all of them.  The unrolled driver below is that
+ *     loop with the gradients supplied from outside.
+ *   - Sec. 2.3 "Memory-efficient and cache-friendly PyTree" and Appendix D,
+ *     Table 2 ("Tree Flatten", "Tree UnFlatten"): flattening a tree into one
+ *     buffer and splitting it back.  pack/unpack below are the definition:
+ *     leaf j occupies flat elements [off_j, off_j + numel_j), row-major.
+ *
+ * Readings where the paper is silent (each also listed in the design notes):
+ *   R1  count = number of steps already taken; bias correction uses
+ *       t = count + 1, c1 = 1 - b1^t, c2 = 1 - b2^t.
+ *   R2  params_out = params + update (apply_updates fused into the step);
+ *       the cotangent of the update equals the cotangent of params_out.
+ *   R3  the 0/0 case: s = sqrt(v_hat + eps_root) = 0 happens only when
+ *       eps_root = 0, v = 0 and g = 0.  There the P-bar contribution to the
+ *       nu cotangent is defined as 0.  The resulting d/dg is the symmetric
+ *       (two-sided mean) derivative of the update at g = 0.
+ *
+ * Parity pins (tests that tie this file to something other than itself):
+ *   forward : step-1 closed form; constant-gradient bias-correction invariant;
+ *             b1 = b2 = 0 special case; gradient-scale invariance;
+ *             torch.optim.Adam in fp64 at eps_root = 0 over many steps.
+ *   backward: step-1 closed form; linearity in the cotangents; autograd
+ *             through torch.optim's functional Adam (differentiable mode) in
+ *             fp64; fp64 central differences of the forward, including the
+ *             symmetric difference at g = 0 (reading R3).
+ *   unrolled: fp64 central differences of the K-step map.
+ *   pack    : numpy concatenation, bit for bit; unpack(pack(x)) == x.
+ *   mag_*   : the tolerance scales are sums of absolute values of terms and
+ *             are checked to bound |value| (triangle inequality).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <string.h>
+
+/* Bias-correction denominators, reading R1. */
+static void bias_corrections(int64_t count, double b1, double b2,
+                             double* c1, double* c2) {
+  double t = (double)(count + 1);
+  *c1 = 1.0 - pow(b1, t);
+  *c2 = 1.0 - pow(b2, t);
+}
+
+/*
+ * One Adam step (Kingma & Ba, Algorithm 1; reading R2 for params_out),
+ * element by element:
+ *   m' = b1 m + (1-b1) g            v' = b2 v + (1-b2) g^2
+ *   m^ = m'/c1                      v^ = v'/c2
+ *   s  = sqrt(v^ + eps_root)        d  = s + eps
+ *   u  = -lr m^ / d                 p' = p + u
+ * u_out may be NULL.
+ */
+void oracle_adam_fwd(int64_t n, const double* p, const double* g,
+                     const double* m, const double* v, int64_t count,
+                     double lr, double b1, double b2, double eps,
+                     double eps_root, double* p_out, double* m_out,
+                     double* v_out, double* u_out) {
+  double c1, c2;
+  bias_corrections(count, b1, b2, &c1, &c2);
+  for (int64_t i = 0; i < n; ++i) {
+    double m1 = b1 * m[i] + (1.0 - b1) * g[i];
+    double v1 = b2 * v[i] + (1.0 - b2) * g[i] * g[i];
+    double mh = m1 / c1;
+    double vh = v1 / c2;
+    double s = sqrt(vh + eps_root);
+    double d = s + eps;
+    double u = -lr * mh / d;
+    m_out[i] = m1;
+    v_out[i] = v1;
+    if (u_out) u_out[i] = u;
+    p_out[i] = p[i] + u;
+  }
+}
+
+/*
+ * Vector-Jacobian product of oracle_adam_fwd (Sec. 2.3: the backward of the
+ * fused optimizer), plain chain rule through the forward's own steps.
+ * Cotangents: dP on p', dM on m', dV on v' (dM, dV may be NULL = zero).
+ *   dL/dm' = Mt = dM - dP lr / (c1 d)
+ *   dL/dv' = Vt = dV + dP lr m^ / (2 c2 s d^2)      (dP term := 0 if s == 0, R3)
+ *   dp = dP
+ *   dg = (1-b1) Mt + 2 (1-b2) g Vt
+ *   dm = b1 Mt
+ *   dv = b2 Vt
+ * dp_out may be NULL (it is the identity on dP).
+ */
+void oracle_adam_bwd(int64_t n, const double* dP, const double* dM,
+                     const double* dV, const double* g, const double* m,
+                     const double* v, int64_t count, double lr, double b1,
+                     double b2, double eps, double eps_root, double* dp_out,
+                     double* dg_out, double* dm_out, double* dv_out) {
+  double c1, c2;
+  bias_corrections(count, b1, b2, &c1, &c2);
+  for (int64_t i = 0; i < n; ++i) {
+    double m1 = b1 * m[i] + (1.0 - b1) * g[i];
+    double v1 = b2 * v[i] + (1.0 - b2) * g[i] * g[i];
+    double mh = m1 / c1;
+    double vh = v1 / c2;
+    double s = sqrt(vh + eps_root);
+    double d = s + eps;
+    double dMi = dM ? dM[i] : 0.0;
+    double dVi = dV ? dV[i] : 0.0;
+    double Mt = dMi - dP[i] * lr / (c1 * d);
+    double Vt = dVi;
+    if (s > 0.0) Vt += dP[i] * lr * mh / (2.0 * c2 * s * d * d);
+    if (dp_out) dp_out[i] = dP[i];
+    dg_out[i] = (1.0 - b1) * Mt + 2.0 * (1.0 - b2) * g[i] * Vt;
+    dm_out[i] = b1 * Mt;
+    dv_out[i] = b2 * Vt;
+  }
+}
+
+/*
+ * Tolerance scales for the forward outputs: for each output, the sum of the
+ * absolute values of the terms that make it up.  A result computed with
+ * relative rounding error r per operation differs from the exact value by a
+ * small multiple of r times this scale, whatever cancellation occurs.
+ *   mag(m') = b1|m| + (1-b1)|g|
+ *   mag(v') = b2|v| + (1-b2) g^2
+ *   mag(u)  = lr mag(m') / (c1 d)
+ *   mag(p') = |p| + mag(u)
+ */
+void oracle_adam_fwd_mag(int64_t n, const double* p, const double* g,
+                         const double* m, const double* v, int64_t count,
+                         double lr, double b1, double b2, double eps,
+                         double eps_root, double* mag_p, double* mag_m,
+                         double* mag_v, double* mag_u) {
+  double c1, c2;
+  bias_corrections(count, b1, b2, &c1, &c2);
+  for (int64_t i = 0; i < n; ++i) {
+    double v1 = b2 * v[i] + (1.0 - b2) * g[i] * g[i];
+    double s = sqrt(v1 / c2 + eps_root);
+    double d = s + eps;
+    double am = b1 * fabs(m[i]) + (1.0 - b1) * fabs(g[i]);
+    double av = b2 * fabs(v[i]) + (1.0 - b2) * g[i] * g[i];
+    double au = lr * am / (c1 * d);
+    mag_m[i] = am;
+    mag_v[i] = av;
+    mag_u[i] = au;
+    mag_p[i] = fabs(p[i]) + au;
+  }
+}
+
+/*
+ * Tolerance scales for the backward outputs.  For dg the scale is taken from
+ * the algebraically reduced form of the same quantity, in which the g^2 terms
+ * of the plain chain rule cancel exactly (substitute v^ = b2 v/c2 + b g^2 and
+ * m^ = b1 m/c1 + a g, with a = (1-b1)/c1, b = (1-b2)/c2):
+ *   dg = (1-b1) dM + 2(1-b2) g dV + dP lr N / (s d^2),
+ *   N  = b b1 g m / c1 - a b2 v / c2 - a (eps_root + s eps);
+ * at s == 0 the dP term is -dP lr a / d (reading R3).
+ *   mag(dg) = (1-b1)|dM| + 2(1-b2)|g dV|
+ *             + |dP| lr (b b1 |g m|/c1 + a b2 |v|/c2 + a (eps_root + s eps)) / (s d^2)
+ *   mag(dm) = b1 (|dM| + |dP| lr / (c1 d))
+ *   mag(dv) = b2 (|dV| + |dP| lr mag(m^) / (2 c2 s d^2)),  mag(m^) = mag(m')/c1
+ * This is the reduced form written out only to size a tolerance; the values
+ * themselves come from oracle_adam_bwd.
+ */
+void oracle_adam_bwd_mag(int64_t n, const double* dP, const double* dM,
+                         const double* dV, const double* g, const double* m,
+                         const double* v, int64_t count, double lr, double b1,
+                         double b2, double eps, double eps_root,
+                         double* mag_dg, double* mag_dm, double* mag_dv) {
+  double c1, c2;
+  bias_corrections(count, b1, b2, &c1, &c2);
+  double a = (1.0 - b1) / c1;
+  double b = (1.0 - b2) / c2;
+  for (int64_t i = 0; i < n; ++i) {
+    double v1 = b2 * v[i] + (1.0 - b2) * g[i] * g[i];
+    double s = sqrt(v1 / c2 + eps_root);
+    double d = s + eps;
+    double adP = fabs(dP[i]);
+    double adM = dM ? fabs(dM[i]) : 0.0;
+    double adV = dV ? fabs(dV[i]) : 0.0;
+    double amh = (b1 * fabs(m[i]) + (1.0 - b1) * fabs(g[i])) / c1;
+    double t3, tv;
+    if (s > 0.0) {
+      double num = b * b1 * fabs(g[i] * m[i]) / c1 + a * b2 * fabs(v[i]) / c2 +
+                   a * (eps_root + s * eps);
+      t3 = adP * lr * num / (s * d * d);
+      tv = adP * lr * amh / (2.0 * c2 * s * d * d);
+    } else {
+      t3 = adP * lr * a / d;
+      tv = 0.0;
+    }
+    mag_dg[i] = (1.0 - b1) * adM + 2.0 * (1.0 - b2) * fabs(g[i]) * adV + t3;
+    mag_dm[i] = b1 * (adM + adP * lr / (c1 * d));
+    mag_dv[i] = b2 * (adV + tv);
+  }
+}
+
+/*
+ * K-step unrolled forward (Listing 1's inner loop with given gradients):
+ *   for k = 1..K: (p_k, m_k, v_k) = step(p_{k-1}, g_k, m_{k-1}, v_{k-1},
+ *                                        count0 + k - 1)
+ * grads: K*n row-major (step k at grads + (k-1)*n).
+ * m_traj, v_traj: (K+1)*n; entry 0 is a copy of m0 / v0, entry k is m_k / v_k.
+ * p_out: p_K.
+ */
+void oracle_unrolled_fwd(int64_t K, int64_t n, const double* p0,
+                         const double* grads, const double* m0,
+                         const double* v0, int64_t count0, double lr,
+                         double b1, double b2, double eps, double eps_root,
+                         double* p_out, double* m_traj, double* v_traj) {
+  memcpy(m_traj, m0, (size_t)n * sizeof(double));
+  memcpy(v_traj, v0, (size_t)n * sizeof(double));
+  memcpy(p_out, p0, (size_t)n * sizeof(double));
+  for (int64_t k = 1; k <= K; ++k) {
+    oracle_adam_fwd(n, p_out, grads + (k - 1) * n, m_traj + (k - 1) * n,
+                    v_traj + (k - 1) * n, count0 + k - 1, lr, b1, b2, eps,
+                    eps_root, p_out, m_traj + k * n, v_traj + k * n, NULL);
+  }
+}
+
+/*
+ * K-step unrolled backward: reverse-mode through the K steps of
+ * oracle_unrolled_fwd, starting from the cotangent dpK of p_K and zero
+ * cotangents of m_K, v_K.
+ *   for k = K..1: (dP, dg_k, dM, dV) = vjp_k(dP, dM, dV)
+ * Outputs: dp0 (= dpK, the params path is the identity), dg (K*n, step k at
+ * dg + (k-1)*n), dm0, dv0.  Inputs m_traj/v_traj as written by the forward.
+ */
+void oracle_unrolled_bwd(int64_t K, int64_t n, const double* dpK,
+                         const double* grads, const double* m_traj,
+                         const double* v_traj, int64_t count0, double lr,
+                         double b1, double b2, double eps, double eps_root,
+                         double* dp0, double* dg, double* dm0, double* dv0) {
+  memcpy(dp0, dpK, (size_t)n * sizeof(double));
+  for (int64_t i = 0; i < n; ++i) {
+    dm0[i] = 0.0;
+    dv0[i] = 0.0;
+  }
+  for (int64_t k = K; k >= 1; --k) {
+    /* dm0/dv0 hold the cotangents of m_k/v_k on entry, of m_{k-1}/v_{k-1}
+       on exit; each element is read before it is written. */
+    oracle_adam_bwd(n, dp0, dm0, dv0, grads + (k - 1) * n,
+                    m_traj + (k - 1) * n, v_traj + (k - 1) * n,
+                    count0 + k - 1, lr, b1, b2, eps, eps_root, dp0,
+                    dg + (k - 1) * n, dm0, dv0);
+  }
+}
+
+/*
+ * Tree pack (flatten), by definition: for every segment j,
+ *   flat[off_j + i] = leaf_j[i],  0 <= i < numel_j,
+ * copied as bytes (elem_bytes per element), so every bit pattern survives.
+ * offsets == NULL means dense: off_j = sum of numel over segments before j.
+ */
+void oracle_pack(int64_t nseg, const int64_t* numel, const int64_t* offsets,
+                 int64_t elem_bytes, const void* const* leaves, void* flat) {
+  int64_t run = 0;
+  for (int64_t j = 0; j < nseg; ++j) {
+    int64_t off = offsets ? offsets[j] : run;
+    memcpy((char*)flat + off * elem_bytes, leaves[j],
+           (size_t)(numel[j] * elem_bytes));
+    run += numel[j];
+  }
+}
+
+/* Tree unpack (unflatten), the mirror: leaf_j[i] = flat[off_j + i]. */
+void oracle_unpack(int64_t nseg, const int64_t* numel, const int64_t* offsets,
+                   int64_t elem_bytes, const void* flat, void* const* leaves) {
+  int64_t run = 0;
+  for (int64_t j = 0; j < nseg; ++j) {
+    int64_t off = offsets ? offsets[j] : run;
+    memcpy(leaves[j], (const char*)flat + off * elem_bytes,
+           (size_t)(numel[j] * elem_bytes));
+    run += numel[j];
+  }
+}
