@@ -1,0 +1,349 @@
+"""Benchmark of the differentiable-Adam hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+  tree flatten of the params tree and of K gradient trees
+  -> K-step unrolled Adam forward (K fused fwd kernels, trajectory kept)
+  -> K-step unrolled Adam backward (K fused VJP kernels, meta-gradient)
+  -> tree unflatten of p_K and of the K gradient cotangents.
+Default workload: the many-small-tensor tree (20,000 fp32 leaves, log-uniform
+sizes in [1, 65536], K = 3).  All inputs are resident in HBM before timing.
+
+Prints ONE JSON line.  `value` is Adam fwd+bwd parameter-steps per second for
+the whole pass (n * K / step time); `roofline` covers the dominant kernel
+(by time), timed with HIP events on the launch stream around its launches.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same work.
+
+    python bench.py [--steps 20] [--warmup 3] [--workload many_small]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD published figure
+METRIC = "diff-Adam fwd+bwd params/s and achieved HBM GB/s (% of MI355X peak), 1 GPU"
+
+# algorithmic bytes per element (fp32): what the method must read + write
+B_FWD = 28          # p, g, m, v -> p', m', v'
+B_BWD = 36          # dP, dM, dV, g, m, v -> dg, dm, dv
+B_BWD_FIRST = 28    # dM = dV = 0: dP, g, m, v -> dg, dm, dv
+B_COPY = 8          # pack / unpack: read once, write once
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="many_small", choices=["many_small", "flat_1b"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2211_06934_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(kernel, workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel, workload))
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_src_sha") != kernel_source_sha():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+# --------------------------------------------------------------------- setup
+
+
+def setup_many_small(torch, P, w):
+    from workloads import HYPER, torch_normal
+    K, n, numel = w.K, w.n, w.numels
+    dev = "cuda"
+
+    def tree_from(flat):  # separately allocated leaves holding flat's values
+        return [x.clone() for x in torch.split(flat, numel)]
+
+    def ptrs(leaves):
+        return torch.tensor([x.data_ptr() for x in leaves], dtype=torch.int64).to(dev)
+
+    p_tree = tree_from(torch_normal(n, 0.05, 101, dev))
+    g_trees = [tree_from(torch_normal(n, w.grad_std, 110 + k, dev)) for k in range(K)]
+    pK_tree = [torch.empty_like(x) for x in p_tree]
+    dg_trees = [[torch.empty_like(x) for x in p_tree] for _ in range(K)]
+    table = P.segtable_create(numel)
+    assert table.total == n
+    z = lambda: torch.zeros(n, dtype=torch.float32, device=dev)  # noqa: E731
+    e = lambda: torch.empty(n, dtype=torch.float32, device=dev)  # noqa: E731
+    S = dict(
+        K=K, n=n, table=table, hyper=dict(HYPER, eps_root=w.eps_root), count0=w.count0,
+        p_ptrs=ptrs(p_tree), g_ptrs=[ptrs(t) for t in g_trees],
+        pK_ptrs=ptrs(pK_tree), dg_ptrs=[ptrs(t) for t in dg_trees],
+        p0=e(), g=[e() for _ in range(K)], mu=[z()] + [e() for _ in range(K)],
+        nu=[z()] + [e() for _ in range(K)], pK=e(), cot=torch_normal(n, 1.0, 120, dev),
+        dg=[e() for _ in range(K)], dm0=e(), dv0=e(),
+        keep=(p_tree, g_trees, pK_tree, dg_trees),
+    )
+    return S
+
+
+def step_many_small(P, S, ev=None):
+    """One pass; if ev is given, records ev[0..4] around the four phases."""
+    h = S["hyper"]
+    args = (S["count0"], h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+    if ev:
+        ev[0].record()
+    P.tree_flatten(S["table"], S["p_ptrs"], S["p0"])
+    for k in range(S["K"]):
+        P.tree_flatten(S["table"], S["g_ptrs"][k], S["g"][k])
+    if ev:
+        ev[1].record()
+    P.adam_unrolled_fwd(S["p0"], S["g"], S["mu"], S["nu"], S["pK"], *args)
+    if ev:
+        ev[2].record()
+    P.adam_unrolled_bwd(S["cot"], S["g"], S["mu"], S["nu"], S["dg"], S["dm0"], S["dv0"], *args)
+    if ev:
+        ev[3].record()
+    P.tree_unflatten(S["table"], S["pK"], S["pK_ptrs"])
+    for k in range(S["K"]):
+        P.tree_unflatten(S["table"], S["dg"][k], S["dg_ptrs"][k])
+    if ev:
+        ev[4].record()
+
+
+def phases_many_small(S):
+    """(name, kernel, launches per step, algorithmic bytes per step) per phase."""
+    K, n = S["K"], S["n"]
+    return [
+        ("flatten", "tree_flatten", K + 1, (K + 1) * B_COPY * n),
+        ("adam_fwd", "adam_fwd", K, K * B_FWD * n),
+        ("adam_bwd", "adam_bwd", K, (B_BWD_FIRST + (K - 1) * B_BWD) * n),
+        ("unflatten", "tree_unflatten", K + 1, (K + 1) * B_COPY * n),
+    ]
+
+
+def setup_flat_1b(torch, P, w):
+    from workloads import HYPER, torch_normal
+    n, dev = w.n, "cuda"
+    S = dict(K=1, n=n, hyper=dict(HYPER, eps_root=w.eps_root), count0=w.count0,
+             p=torch_normal(n, 0.05, 201, dev), g=torch_normal(n, w.grad_std, 202, dev),
+             m=torch_normal(n, 1e-4, 203, dev).abs_(), v=torch_normal(n, 1e-4, 204, dev).abs_(),
+             dP=torch_normal(n, 1.0, 205, dev), dM=torch_normal(n, 1.0, 206, dev),
+             dV=torch_normal(n, 1.0, 207, dev))
+    for k in ("po", "mo", "vo", "dg", "dm", "dv"):
+        S[k] = torch.empty(n, dtype=torch.float32, device=dev)
+    return S
+
+
+def step_flat_1b(P, S, ev=None):
+    h = S["hyper"]
+    args = (S["count0"], h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+    if ev:
+        ev[0].record()
+    P.adam_fwd(S["p"], S["g"], S["m"], S["v"], *args, S["po"], S["mo"], S["vo"])
+    if ev:
+        ev[1].record()
+    P.adam_bwd(S["dP"], S["dM"], S["dV"], S["g"], S["m"], S["v"], *args, None, S["dg"], S["dm"], S["dv"])
+    if ev:
+        ev[2].record()
+
+
+def phases_flat_1b(S):
+    n = S["n"]
+    return [("adam_fwd", "adam_fwd", 1, B_FWD * n), ("adam_bwd", "adam_bwd", 1, B_BWD * n)]
+
+
+# ------------------------------------------------------------- CPU baseline
+
+
+def cpu_baseline_many_small(w, target_s):
+    """Time the CPU oracle (single thread) on the first leaves of the tree: pack
+    p and K grads, K-step fwd, K-step bwd, unpack p_K and K cotangents."""
+    import numpy as np
+    import oracle
+    from workloads import HYPER, normal
+    h = dict(HYPER, eps_root=w.eps_root)
+    numel = w.numels
+
+    def run(nleaves):
+        sizes = numel[:nleaves]
+        n = int(sum(sizes))
+        K = w.K
+        flatp = normal(n, 0.05, "cpu", "p0")
+        grads32 = [normal(n, w.grad_std, "cpu", "grad", k) for k in range(K)]
+        leaves_p = np.split(flatp, np.cumsum(sizes)[:-1])
+        leaves_g = [np.split(g, np.cumsum(sizes)[:-1]) for g in grads32]
+        cot = normal(n, 1.0, "cpu", "cot_p").astype(np.float64)
+        z = np.zeros(n)
+        t0 = time.perf_counter()
+        p_flat = oracle.pack(leaves_p)
+        g_flat = [oracle.pack(lg) for lg in leaves_g]
+        t1 = time.perf_counter()
+        p64 = p_flat.astype(np.float64)
+        G = np.stack([g.astype(np.float64) for g in g_flat])
+        t2 = time.perf_counter()
+        pK, mt, vt = oracle.unrolled_fwd(p64, G, z, z, w.count0, h["lr"], h["b1"], h["b2"], h["eps"],
+                                         h["eps_root"])
+        dp0, dg, dm0, dv0 = oracle.unrolled_bwd(cot, G, mt, vt, w.count0, h["lr"], h["b1"], h["b2"], h["eps"],
+                                                h["eps_root"])
+        t3 = time.perf_counter()
+        shapes = [(s,) for s in sizes]
+        oracle.unpack(pK, shapes)
+        for k in range(K):
+            oracle.unpack(dg[k], shapes)
+        t4 = time.perf_counter()
+        return n, (t1 - t0) + (t3 - t2) + (t4 - t3)
+
+    # calibrate on a small prefix, then size the sample to about target_s
+    n_small, t_small = run(200)
+    rate = n_small / max(t_small, 1e-9)
+    want = rate * target_s
+    acc, nleaves = 0, 0
+    for s in numel:
+        if acc >= want:
+            break
+        acc += s
+        nleaves += 1
+    n, t = run(nleaves)
+    return {
+        "value": n * w.K / t, "unit": "params/s", "cores": 1, "kind": "oracle",
+        "sample": "first %d of %d leaves (%d of %d params), whole step: pack p + %d grads, %d-step fwd+bwd, "
+                  "unpack p_K + %d cotangents; fp64 single thread; %.1f s"
+                  % (nleaves, len(numel), n, w.n, w.K, w.K, w.K, t),
+        "seconds": t,
+        "host_cpu": platform.processor() or platform.machine(),
+    }
+
+
+def cpu_baseline_flat_1b(w, target_s):
+    import numpy as np
+    import oracle
+    from workloads import HYPER, abs_normal, normal
+    h = dict(HYPER, eps_root=w.eps_root)
+
+    def run(n):
+        p, g = normal(n, 0.05, "cpu", "p0").astype(np.float64), normal(n, w.grad_std, "cpu", "grad").astype(np.float64)
+        m, v = abs_normal(n, 1e-4, "cpu", "mu").astype(np.float64), abs_normal(n, 1e-4, "cpu", "nu").astype(np.float64)
+        dP, dM, dV = (normal(n, 1.0, "cpu", t).astype(np.float64) for t in ("cot_p", "cot_m", "cot_v"))
+        t0 = time.perf_counter()
+        oracle.adam_fwd(p, g, m, v, w.count0, h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+        oracle.adam_bwd(dP, dM, dV, g, m, v, w.count0, h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+        return time.perf_counter() - t0
+
+    t_small = run(1 << 20)
+    n = int(min(w.n, (1 << 20) / max(t_small, 1e-9) * target_s))
+    t = run(n)
+    return {"value": n / t, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of %d params, one fwd+bwd step; fp64 single thread; %.1f s" % (n, w.n, t),
+            "seconds": t, "host_cpu": platform.processor() or platform.machine()}
+
+
+# ---------------------------------------------------------------------- main
+
+
+def main():
+    a = parse()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        sys.stderr.write("bench.py: this build runs on one GPU only; --gpus %d is not supported "
+                         "(the kernels are elementwise and would shard by contiguous ranges)\n" % a.gpus)
+        sys.exit(2)
+    import torch
+    import paper_2211_06934_amd as P
+    from workloads import WORKLOADS
+    if not torch.cuda.is_available():
+        sys.stderr.write("bench.py: no GPU visible\n")
+        sys.exit(1)
+    w = WORKLOADS[a.workload]()
+    if a.workload == "many_small":
+        S, step, phases = setup_many_small(torch, P, w), step_many_small, phases_many_small
+    else:
+        S, step, phases = setup_flat_1b(torch, P, w), step_flat_1b, phases_flat_1b
+    ph = phases(S)
+    nph = len(ph)
+    torch.cuda.synchronize()
+
+    # a plain copy of known size, outside the timed region: the calibration
+    # point for the HBM byte counters of profiling runs of this same command
+    cal_src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    cal_dst = torch.empty_like(cal_src)
+    cal_dst.copy_(cal_src)
+    torch.cuda.synchronize()
+    del cal_src, cal_dst
+
+    for _ in range(a.warmup):
+        step(P, S)
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)] for _ in range(a.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for s in range(a.steps):
+        step(P, S, evs[s])
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / a.steps
+    phase_ms = [sum(e[i].elapsed_time(e[i + 1]) for e in evs) / a.steps for i in range(nph)]
+
+    n, K = S["n"], S["K"]
+    bytes_step = sum(p[3] for p in ph)
+    value = n * K / (ms_step * 1e-3)
+    gbs = bytes_step / (ms_step * 1e-3) / 1e9
+    breakdown = {}
+    for (name, kern, launches, byts), t in zip(ph, phase_ms):
+        breakdown[name] = {"ms": round(t, 4), "launches": launches, "GB/s": round(byts / (t * 1e-3) / 1e9, 1),
+                           "frac": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    dom = max(range(nph), key=lambda i: phase_ms[i])
+    dname, dkern, dlaunch, dbytes = ph[dom]
+    avg_launch_s = phase_ms[dom] * 1e-3 / dlaunch
+    per_launch_bytes = dbytes / dlaunch
+    achieved = per_launch_bytes / avg_launch_s / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic_from_profile(dkern, a.workload),
+                "kernel": dkern, "bytes_per_launch": int(per_launch_bytes),
+                "avg_launch_us": round(avg_launch_s * 1e6, 2)}
+
+    cpu = None
+    if not a.no_cpu_baseline:
+        cpu = (cpu_baseline_many_small if a.workload == "many_small" else cpu_baseline_flat_1b)(w, a.cpu_seconds)
+        cpu["value"] = float("%.4g" % cpu["value"])
+
+    out = {
+        "metric": METRIC, "value": float("%.6g" % value), "unit": "params/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.description, "n_params": n, "leaves": w.nseg, "K": K,
+                   "step": "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg"
+                   if a.workload == "many_small" else "one Adam fwd + one Adam bwd (count 100, all cotangents)",
+                   "parallelism": "single GPU"},
+        "achieved_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "bytes_per_step": int(bytes_step), "phases": breakdown,
+        "roofline": roofline, "cpu_baseline": cpu,
+        "kernel_src_sha": kernel_source_sha(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,203 @@
+/*
+ * diffopt.h -- C ABI of the MI355X (gfx950) differentiable-Adam hot path.
+ *
+ * The operations are those of TorchOpt (arXiv 2211.06934):
+ *   - Sec. 2.3 "CPU/GPU-accelerated optimizers": the whole Adam optimizer is
+ *     one differentiable operator with a hand-written forward and backward;
+ *   - Listing 1 (explicit gradient): a non-inplace update + apply_updates,
+ *     repeated for a number of inner steps, then one backward pass through
+ *     all of them (the meta-gradient);
+ *   - Sec. 2.3 "Memory-efficient and cache-friendly PyTree" and Appendix D,
+ *     Table 2: tree flatten / unflatten of a parameter tree.
+ * The paper prints no Adam formula; the update is Adam of Kingma & Ba (ICLR
+ * 2015, Algorithm 1) with an extra eps_root inside the square root:
+ *   t = count + 1,  c1 = 1 - b1^t,  c2 = 1 - b2^t
+ *   m' = b1 m + (1-b1) g,   v' = b2 v + (1-b2) g^2
+ *   s  = sqrt(v'/c2 + eps_root),   d = s + eps
+ *   u  = -lr (m'/c1) / d,   p' = p + u
+ *
+ * Conventions shared by every call:
+ *   - Element buffers are device pointers (HBM), fp32 unless stated, and
+ *     owned by the caller; the library never allocates on these paths.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Calls enqueue work on it and return without synchronising; a fault in
+ *     a kernel surfaces at the caller's next synchronisation.
+ *   - Scalars cross the ABI in fp64; the library derives every coefficient
+ *     (1-b1, 1-b2, 1/c1, 1/c2, lr/c1, ...) in fp64 and rounds each once to
+ *     fp32 before the kernels use it.
+ *   - Return value: DIFFOPT_OK or a negative code; the message for the last
+ *     nonzero return on the calling thread is diffopt_last_error().  No call
+ *     aborts the process or throws across the ABI.
+ *   - n == 0 is a valid no-op.
+ *   - 16-byte aligned element pointers take the 128-bit vector path; any
+ *     other (4-byte aligned) pointer takes a scalar path with the same result.
+ */
+#ifndef DIFFOPT_H
+#define DIFFOPT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DIFFOPT_OK 0
+#define DIFFOPT_EINVAL (-1) /* bad argument: null pointer, range, overlap   */
+#define DIFFOPT_ENOMEM (-2) /* host or device allocation failed             */
+#define DIFFOPT_EHIP (-3)   /* a HIP runtime call or kernel launch failed   */
+
+/* Message describing the last nonzero return on this thread ("" if none).
+ * The pointer stays valid until the next diffopt call on the same thread. */
+const char* diffopt_last_error(void);
+
+/* -------------------------------------------------------------------------
+ * Segment table for tree flatten / unflatten (Appendix D, Table 2; Sec. 2.3
+ * "PyTree").  A tree of S leaves maps onto one flat buffer: leaf j occupies
+ * flat elements [off_j, off_j + numel_j), its elements in row-major order.
+ *
+ * The table depends only on the tree's structure (leaf sizes, layout and
+ * element size), so one table serves every tree instance of that structure
+ * (params, each step's grads, ...); leaf addresses are passed per call.
+ */
+typedef struct diffopt_segtable diffopt_segtable;
+
+/* Build a table on the current HIP device.
+ *   nseg        number of leaves S (>= 0)
+ *   numel       host array [nseg], elements per leaf (>= 0; empty leaves ok)
+ *   offsets     host array [nseg] of flat element offsets, or NULL for the
+ *               dense layout off_j = numel_0 + ... + numel_{j-1}.  Explicit
+ *               offsets may leave gaps (untouched by flatten) but the flat
+ *               ranges of nonempty leaves must not overlap (EINVAL).
+ *   elem_bytes  element size in bytes: 1, 2, 4 or 8 (fp32 = 4)
+ *   out         receives the table; the caller frees it with
+ *               diffopt_segtable_destroy.
+ * Copies what it needs; the caller's arrays may be freed on return.  Owns a
+ * small device array (about 32 bytes per nonempty leaf), uploaded
+ * synchronously here.                                                      */
+int diffopt_segtable_create(int64_t nseg, const int64_t* numel,
+                            const int64_t* offsets, int32_t elem_bytes,
+                            diffopt_segtable** out);
+
+/* Free a table and its device memory (NULL is a no-op).  The caller must
+ * make sure no enqueued flatten/unflatten still uses it.                    */
+void diffopt_segtable_destroy(diffopt_segtable* table);
+
+/* Flat length n in elements (max over leaves of off_j + numel_j); -1 if
+ * table is NULL.                                                            */
+int64_t diffopt_segtable_total(const diffopt_segtable* table);
+
+/* Number of leaves S the table was built for; -1 if table is NULL.          */
+int64_t diffopt_segtable_nseg(const diffopt_segtable* table);
+
+/* Tree flatten (pack): flat[off_j + i] = leaf_j[i] for all j, i < numel_j.
+ *   leaf_ptrs   DEVICE array [nseg] of uint64 leaf addresses, in table order
+ *               (entries of empty leaves are ignored and may be 0)
+ *   flat        device buffer of at least diffopt_segtable_total() elements
+ * Copies bits through integer registers: NaN payloads, signed zeros and
+ * subnormals survive.  Pointers must be aligned to elem_bytes.  The flat
+ * buffer must not overlap any leaf.                                         */
+int diffopt_tree_flatten(const diffopt_segtable* table,
+                         const uint64_t* leaf_ptrs, void* flat, void* stream);
+
+/* Tree unflatten (unpack), the mirror: leaf_j[i] = flat[off_j + i].
+ * Leaves must not overlap each other or the flat buffer.                     */
+int diffopt_tree_unflatten(const diffopt_segtable* table, const void* flat,
+                           const uint64_t* leaf_ptrs, void* stream);
+
+/* -------------------------------------------------------------------------
+ * Differentiable Adam step, forward (Sec. 2.3; Listing 1's
+ * opt.update(..., inplace=False) followed by apply_updates, fused).
+ *   params, grad, mu, nu        inputs [n]
+ *   count                       steps already taken (>= 0); bias correction
+ *                               uses t = count + 1; the caller's state
+ *                               becomes count + 1
+ *   lr (finite), b1, b2 in [0, 1), eps >= 0, eps_root >= 0
+ *   params_out, mu_out, nu_out  outputs [n] (p', m', v')
+ *   update_out                  optional output [n] (u = p' - p), or NULL
+ * Each output may alias its own input (params_out == params, ...): every
+ * element is read and then written by one thread.  Writing mu_out/nu_out
+ * over mu/nu destroys what diffopt_adam_bwd needs: that is the
+ * non-differentiable in-place mode.                                         */
+int diffopt_adam_fwd(const float* params, const float* grad, const float* mu,
+                     const float* nu, int64_t n, int64_t count, double lr,
+                     double b1, double b2, double eps, double eps_root,
+                     float* params_out, float* mu_out, float* nu_out,
+                     float* update_out, void* stream);
+
+/* Differentiable Adam step, backward: the vector-Jacobian product of
+ * diffopt_adam_fwd (Sec. 2.3: hand-written backward with symbolic reduction
+ * and explicit cancelling of 0/0 cases).
+ *   dupdate    cotangent of params_out [n] (equal to that of update_out,
+ *              since params_out = params + update)
+ *   dmu, dnu   cotangents of mu_out, nu_out [n], or NULL for zero
+ *   grad, mu, nu   the forward's INPUTS g, m, v (not its outputs)
+ *   count, lr, b1, b2, eps, eps_root   as passed to the forward
+ *   dparams    cotangent of params [n]; the params path is the identity, so
+ *              this is a copy of dupdate; NULL (or == dupdate) skips it
+ *   dgrad, dmu_in, dnu_in   cotangents of grad, mu, nu [n]
+ * dmu_in may alias dmu and dnu_in may alias dnu (read-then-write per
+ * element).  The computation is the algebraically reduced form, in which
+ * the g^2 terms of the plain chain rule cancel exactly:
+ *   a = (1-b1)/c1,  b = (1-b2)/c2
+ *   N = b b1 g m / c1 - a b2 v / c2 - a (eps_root + s eps)
+ *   dgrad  = (1-b1) dmu + 2 (1-b2) g dnu + dupdate lr N / (s d^2)
+ *   dmu_in = b1 (dmu - dupdate lr / (c1 d))
+ *   dnu_in = b2 (dnu + dupdate lr (m'/c1) / (2 c2 s d^2))
+ * At s == 0 (only when eps_root == 0, v == 0 and g == 0) the dupdate term of
+ * dgrad is -dupdate lr a / d (the two-sided mean derivative) and that of
+ * dnu_in is 0.                                                              */
+int diffopt_adam_bwd(const float* dupdate, const float* dmu, const float* dnu,
+                     const float* grad, const float* mu, const float* nu,
+                     int64_t n, int64_t count, double lr, double b1, double b2,
+                     double eps, double eps_root, float* dparams, float* dgrad,
+                     float* dmu_in, float* dnu_in, void* stream);
+
+/* -------------------------------------------------------------------------
+ * K-step unrolled driver, forward (Listing 1's inner loop with the K
+ * gradients given up front):
+ *   for k = 1..K: (p_k, mu_k, nu_k) = adam_fwd(p_{k-1}, grads[k-1],
+ *                                             mu_{k-1}, nu_{k-1}, count0+k-1)
+ *   K >= 1, n >= 0
+ *   p0          input [n] (not modified unless pK == p0)
+ *   grads       HOST array [K] of device pointers, grads[k-1] = g_k
+ *   mu_traj     HOST array [K+1] of device pointers: mu_traj[0] = mu0 is
+ *               read, mu_traj[k] receives mu_k (the trajectory the backward
+ *               needs); all K+1 buffers distinct
+ *   nu_traj     the same for nu
+ *   pK          output [n]; also the running params buffer (steps 2..K
+ *               update it in place)
+ * Enqueues K kernels on `stream`, no host synchronisation.                  */
+int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0,
+                              const float* const* grads,
+                              float* const* mu_traj, float* const* nu_traj,
+                              float* pK, int64_t count0, double lr, double b1,
+                              double b2, double eps, double eps_root,
+                              void* stream);
+
+/* K-step unrolled driver, backward (the meta-gradient of Listing 1's final
+ * autograd.grad): starting from the cotangent dpK of p_K and zero
+ * cotangents of mu_K, nu_K,
+ *   for k = K..1: (dP, dgrads[k-1], dM, dV) = adam_bwd(dP, dM, dV, g_k,
+ *                                   mu_{k-1}, nu_{k-1}, count0+k-1)
+ *   dpK         input [n]; the cotangent of p0 equals dpK (identity), so it
+ *               is not copied
+ *   grads, mu_traj, nu_traj   as given to / written by the forward (HOST
+ *               arrays of device pointers; mu_traj[K], nu_traj[K] unused)
+ *   dgrads      HOST array [K] of device pointers: dgrads[k-1] receives the
+ *               cotangent of g_k
+ *   dmu0, dnu0  outputs [n]: cotangents of mu0, nu0 (used as the running
+ *               dM, dV buffers, updated in place)
+ * Enqueues K kernels on `stream`, the first with zero dM, dV.               */
+int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
+                              const float* const* grads,
+                              const float* const* mu_traj,
+                              const float* const* nu_traj,
+                              float* const* dgrads, float* dmu0, float* dnu0,
+                              int64_t count0, double lr, double b1, double b2,
+                              double eps, double eps_root, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DIFFOPT_H */

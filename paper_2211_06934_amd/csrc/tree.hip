@@ -1,0 +1,326 @@
+// Tree flatten / unflatten through a segment table on gfx950 (TorchOpt,
+// Sec. 2.3 "Memory-efficient and cache-friendly PyTree"; Appendix D, Table 2).
+//
+// Work decomposition.  Every copy writes whole, naturally aligned 16-byte
+// vectors of its DESTINATION (the flat buffer for flatten, the leaves for
+// unflatten).  Nonempty leaf j owns G_j = ceil(bytes_j / 16) + 1 consecutive
+// "groups" of a global group index space; group k of leaf j is the aligned
+// 16-byte destination vector number k counted from the vector that holds the
+// leaf's first destination byte.  The +1 covers any alignment phase, so the
+// G_j groups always cover the leaf; a group may be partial (head, tail) or
+// empty.  Each lane owns one group per step: full groups take one aligned
+// 128-bit store, fed by one or two aligned 128-bit loads of the source and a
+// funnel shift when source and destination phases differ (dense offsets put
+// ~3/4 of leaves out of phase with their flat range); partial groups copy
+// element by element.  Every byte is copied through integer registers, so NaN
+// payloads, signed zeros and subnormals survive.
+//
+// Segment lookup.  Block b handles groups [b*TG, (b+1)*TG).  The host
+// precomputes tile_first[b], the leaf holding group b*TG; the leaves a tile
+// touches are the window tile_first[b] .. tile_first[b+1].  The block stages
+// that window (group offsets, flat offsets, byte sizes, leaf addresses) in LDS
+// once, then every lane binary-searches the LDS window for its group.  Since
+// every nonempty leaf owns >= 2 groups, a window never exceeds TG/2 + 2
+// leaves, which bounds the LDS footprint.
+//
+// Page safety of the two source loads: a full group's 16 source bytes are all
+// valid leaf bytes, the first aligned source vector contains the first of them
+// and the second contains the last, and an aligned 16-byte vector never spans
+// two pages, so neither load touches a page the copy does not already use.
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "common.hpp"
+
+#ifndef DIFFOPT_TREE_U
+#define DIFFOPT_TREE_U 2  // groups (16-byte vectors) per lane per tile
+#endif
+
+namespace diffopt {
+namespace {
+
+constexpr int kTreeU = DIFFOPT_TREE_U;
+constexpr int64_t kTileGroups = (int64_t)kBlock * kTreeU;
+constexpr int kWindowMax = (int)(kTileGroups / 2 + 2);
+
+// One nonempty leaf, in table order.  The entry after the last nonempty leaf
+// is a sentinel whose goff is the total group count.
+struct SegEntry {
+  int64_t goff;   // first group index
+  int64_t off;    // flat element offset
+  int64_t numel;  // elements
+  int64_t orig;   // index into the caller's leaf-address array
+};
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int E>
+struct ElemT;
+template <>
+struct ElemT<1> {
+  typedef uint8_t T;
+};
+template <>
+struct ElemT<2> {
+  typedef uint16_t T;
+};
+template <>
+struct ElemT<4> {
+  typedef uint32_t T;
+};
+template <>
+struct ElemT<8> {
+  typedef uint64_t T;
+};
+
+__device__ __forceinline__ uint32_t pick4(uint32_t a, uint32_t b, uint32_t c, uint32_t d, uint32_t q) {
+  return q == 0 ? a : (q == 1 ? b : (q == 2 ? c : d));
+}
+
+// The 16 bytes starting s bytes into the 32-byte window (w0, w1), 0 < s < 16.
+template <int E>
+__device__ __forceinline__ u32x4 funnel(u32x4 w0, u32x4 w1, uint32_t s) {
+  const uint32_t q = s >> 2;
+  if (E >= 4) {  // s is a multiple of 4: whole-dword selection, q in 1..3
+    u32x4 o;
+    o.x = q == 1 ? w0.y : (q == 2 ? w0.z : w0.w);
+    o.y = q == 1 ? w0.z : (q == 2 ? w0.w : w1.x);
+    o.z = q == 1 ? w0.w : (q == 2 ? w1.x : w1.y);
+    o.w = q == 1 ? w1.x : (q == 2 ? w1.y : w1.z);
+    return o;
+  } else {
+    const uint32_t r = s & 3u;
+    const uint32_t y0 = pick4(w0.x, w0.y, w0.z, w0.w, q);
+    const uint32_t y1 = pick4(w0.y, w0.z, w0.w, w1.x, q);
+    const uint32_t y2 = pick4(w0.z, w0.w, w1.x, w1.y, q);
+    const uint32_t y3 = pick4(w0.w, w1.x, w1.y, w1.z, q);
+    const uint32_t y4 = pick4(w1.x, w1.y, w1.z, w1.w, q);
+    u32x4 o;
+    o.x = __builtin_amdgcn_alignbyte(y1, y0, r);
+    o.y = __builtin_amdgcn_alignbyte(y2, y1, r);
+    o.z = __builtin_amdgcn_alignbyte(y3, y2, r);
+    o.w = __builtin_amdgcn_alignbyte(y4, y3, r);
+    return o;
+  }
+}
+
+template <int E, bool PACK>
+__global__ __launch_bounds__(kBlock) void tree_copy_kernel(const SegEntry* __restrict__ seg,
+                                                           const int64_t* __restrict__ tile_first,
+                                                           int64_t ngroups, const uint64_t* __restrict__ leaf_ptrs,
+                                                           uint64_t flat) {
+  __shared__ int64_t s_goff[kWindowMax + 1];
+  __shared__ int64_t s_fbase[kWindowMax];  // flat byte address of the leaf's range
+  __shared__ int64_t s_bytes[kWindowMax];
+  __shared__ uint64_t s_leaf[kWindowMax];
+
+  const int64_t b = blockIdx.x;
+  const int64_t j0 = tile_first[b];
+  const int W = (int)(tile_first[b + 1] - j0 + 1);
+  for (int t = threadIdx.x; t <= W; t += kBlock) {
+    const SegEntry e = seg[j0 + t];
+    s_goff[t] = e.goff;
+    if (t < W) {
+      s_fbase[t] = (int64_t)(flat + (uint64_t)(e.off * E));
+      s_bytes[t] = e.numel * E;
+      s_leaf[t] = leaf_ptrs[e.orig];
+    }
+  }
+  __syncthreads();
+
+  typedef typename ElemT<E>::T T;
+#pragma unroll
+  for (int u = 0; u < kTreeU; ++u) {
+    const int64_t gidx = b * kTileGroups + (int64_t)u * kBlock + threadIdx.x;
+    if (gidx >= ngroups) break;
+    // largest t with s_goff[t] <= gidx; s_goff[0] <= gidx holds by construction
+    int lo = 0, hi = W - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_goff[mid] <= gidx) lo = mid;
+      else hi = mid - 1;
+    }
+    const uint64_t k = (uint64_t)(gidx - s_goff[lo]);
+    const uint64_t fb = (uint64_t)s_fbase[lo];
+    const uint64_t lb = s_leaf[lo];
+    const uint64_t nb = (uint64_t)s_bytes[lo];
+    const uint64_t dst0 = PACK ? fb : lb;
+    const uint64_t src0 = PACK ? lb : fb;
+    const uint64_t A = (dst0 & ~uint64_t(15)) + 16u * k;
+    const uint64_t lo_b = A > dst0 ? A : dst0;
+    const uint64_t hi_b = (A + 16u) < (dst0 + nb) ? (A + 16u) : (dst0 + nb);
+    if (lo_b >= hi_b) continue;
+    const uint64_t delta = src0 - dst0;  // modular; source byte of x is x + delta
+    if (lo_b == A && hi_b == A + 16u) {
+      const uint64_t S = A + delta;
+      const uint32_t s = (uint32_t)(S & 15u);
+      const u32x4* L = reinterpret_cast<const u32x4*>(S - s);
+      u32x4 out = L[0];
+      if (s != 0) out = funnel<E>(out, L[1], s);
+      *reinterpret_cast<u32x4*>(A) = out;
+    } else {
+      for (uint64_t x = lo_b; x < hi_b; x += E) {
+        *reinterpret_cast<T*>(x) = *reinterpret_cast<const T*>(x + delta);
+      }
+    }
+  }
+}
+
+}  // namespace
+}  // namespace diffopt
+
+using namespace diffopt;
+
+struct diffopt_segtable {
+  int64_t nseg = 0;
+  int64_t total = 0;
+  int64_t nact = 0;
+  int64_t ngroups = 0;
+  int64_t ntiles = 0;
+  int32_t elem_bytes = 4;
+  int device = 0;
+  SegEntry* d_seg = nullptr;       // [nact + 1]
+  int64_t* d_tile_first = nullptr;  // [ntiles + 1]
+};
+
+extern "C" int diffopt_segtable_create(int64_t nseg, const int64_t* numel, const int64_t* offsets,
+                                       int32_t elem_bytes, diffopt_segtable** out) {
+  clear_error();
+  static const char* who = "diffopt_segtable_create";
+  if (!out) return fail(DIFFOPT_EINVAL, "%s: out is NULL", who);
+  *out = nullptr;
+  if (nseg < 0) return fail(DIFFOPT_EINVAL, "%s: nseg must be >= 0", who);
+  if (nseg > 0 && !numel) return fail(DIFFOPT_EINVAL, "%s: numel is NULL", who);
+  if (elem_bytes != 1 && elem_bytes != 2 && elem_bytes != 4 && elem_bytes != 8)
+    return fail(DIFFOPT_EINVAL, "%s: elem_bytes must be 1, 2, 4 or 8 (got %d)", who, elem_bytes);
+  const int64_t kMaxElems = (int64_t(1) << 58) / elem_bytes;
+
+  std::vector<SegEntry> host;
+  std::vector<std::pair<int64_t, int64_t>> ranges;  // (off, end) of nonempty leaves
+  try {
+    host.reserve((size_t)nseg + 1);
+    ranges.reserve((size_t)nseg);
+  } catch (const std::bad_alloc&) {
+    return fail(DIFFOPT_ENOMEM, "%s: host allocation failed", who);
+  }
+  int64_t run = 0, total = 0, goff = 0;
+  for (int64_t j = 0; j < nseg; ++j) {
+    const int64_t k = numel[j];
+    if (k < 0) return fail(DIFFOPT_EINVAL, "%s: numel[%lld] < 0", who, (long long)j);
+    if (k > kMaxElems) return fail(DIFFOPT_EINVAL, "%s: numel[%lld] too large", who, (long long)j);
+    const int64_t off = offsets ? offsets[j] : run;
+    if (off < 0 || off > kMaxElems - k)
+      return fail(DIFFOPT_EINVAL, "%s: offset of leaf %lld out of range", who, (long long)j);
+    run = off + k;
+    if (k == 0) continue;
+    total = std::max(total, off + k);
+    const int64_t groups = (k * elem_bytes + 15) / 16 + 1;
+    host.push_back(SegEntry{goff, off, k, j});
+    ranges.emplace_back(off, off + k);
+    goff += groups;
+  }
+  if (offsets) {
+    std::sort(ranges.begin(), ranges.end());
+    for (size_t i = 1; i < ranges.size(); ++i)
+      if (ranges[i].first < ranges[i - 1].second)
+        return fail(DIFFOPT_EINVAL, "%s: flat ranges of two leaves overlap at element %lld", who,
+                    (long long)ranges[i].first);
+  }
+  const int64_t nact = (int64_t)host.size();
+  host.push_back(SegEntry{goff, 0, 0, 0});  // sentinel
+
+  diffopt_segtable* t = new (std::nothrow) diffopt_segtable();
+  if (!t) return fail(DIFFOPT_ENOMEM, "%s: host allocation failed", who);
+  t->nseg = nseg;
+  t->total = total;
+  t->nact = nact;
+  t->ngroups = goff;
+  t->elem_bytes = elem_bytes;
+  t->ntiles = (goff + kTileGroups - 1) / kTileGroups;
+  hipGetDevice(&t->device);
+
+  std::vector<int64_t> tf;
+  if (t->ntiles > 0) {
+    tf.resize((size_t)t->ntiles + 1);
+    // tile_first[b] = the leaf whose group range holds group b*TG
+    int64_t j = 0;
+    for (int64_t b = 0; b < t->ntiles; ++b) {
+      const int64_t g = b * kTileGroups;
+      while (j + 1 < nact && host[(size_t)j + 1].goff <= g) ++j;
+      tf[(size_t)b] = j;
+    }
+    tf[(size_t)t->ntiles] = nact - 1;
+    hipError_t e = hipMalloc(reinterpret_cast<void**>(&t->d_seg), sizeof(SegEntry) * host.size());
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&t->d_tile_first), sizeof(int64_t) * tf.size());
+    if (e == hipSuccess)
+      e = hipMemcpy(t->d_seg, host.data(), sizeof(SegEntry) * host.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy(t->d_tile_first, tf.data(), sizeof(int64_t) * tf.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      int code = (e == hipErrorOutOfMemory) ? DIFFOPT_ENOMEM : DIFFOPT_EHIP;
+      diffopt_segtable_destroy(t);
+      return fail(code, "%s: %s", who, hipGetErrorString(e));
+    }
+  }
+  *out = t;
+  return DIFFOPT_OK;
+}
+
+extern "C" void diffopt_segtable_destroy(diffopt_segtable* t) {
+  if (!t) return;
+  if (t->d_seg) hipFree(t->d_seg);
+  if (t->d_tile_first) hipFree(t->d_tile_first);
+  delete t;
+}
+
+extern "C" int64_t diffopt_segtable_total(const diffopt_segtable* t) { return t ? t->total : -1; }
+
+extern "C" int64_t diffopt_segtable_nseg(const diffopt_segtable* t) { return t ? t->nseg : -1; }
+
+namespace {
+
+template <bool PACK>
+int tree_copy(const char* who, const diffopt_segtable* t, const uint64_t* leaf_ptrs, uint64_t flat, void* stream) {
+  if (!t) return fail(DIFFOPT_EINVAL, "%s: table is NULL", who);
+  if (t->ntiles == 0) return DIFFOPT_OK;
+  if (!leaf_ptrs || !flat) return fail(DIFFOPT_EINVAL, "%s: null leaf_ptrs or flat", who);
+  if (flat % (uint64_t)t->elem_bytes != 0)
+    return fail(DIFFOPT_EINVAL, "%s: flat is not aligned to elem_bytes", who);
+  hipStream_t st = as_stream(stream);
+  dim3 grid((unsigned)t->ntiles), block(kBlock);
+  switch (t->elem_bytes) {
+    case 1:
+      hipLaunchKernelGGL((tree_copy_kernel<1, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
+                         leaf_ptrs, flat);
+      break;
+    case 2:
+      hipLaunchKernelGGL((tree_copy_kernel<2, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
+                         leaf_ptrs, flat);
+      break;
+    case 4:
+      hipLaunchKernelGGL((tree_copy_kernel<4, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
+                         leaf_ptrs, flat);
+      break;
+    default:
+      hipLaunchKernelGGL((tree_copy_kernel<8, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
+                         leaf_ptrs, flat);
+      break;
+  }
+  return launch_status(who);
+}
+
+}  // namespace
+
+extern "C" int diffopt_tree_flatten(const diffopt_segtable* t, const uint64_t* leaf_ptrs, void* flat, void* stream) {
+  clear_error();
+  return tree_copy<true>("diffopt_tree_flatten", t, leaf_ptrs, reinterpret_cast<uint64_t>(flat), stream);
+}
+
+extern "C" int diffopt_tree_unflatten(const diffopt_segtable* t, const void* flat, const uint64_t* leaf_ptrs,
+                                      void* stream) {
+  clear_error();
+  return tree_copy<false>("diffopt_tree_unflatten", t, leaf_ptrs, reinterpret_cast<uint64_t>(flat), stream);
+}

@@ -1,0 +1,225 @@
+"""Python binding of the diffopt C ABI (include/diffopt.h).
+
+Argument marshalling only: every function here is the C entry point
+``diffopt_<name>`` with the same arguments, taking torch tensors (device
+memory) or raw device addresses, and enqueuing on the current torch stream
+unless a stream is given.  All arithmetic and data movement happens in the
+HIP library; importing this module fails loudly if the library is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdiffopt.so")
+
+DIFFOPT_OK = 0
+DIFFOPT_EINVAL = -1
+DIFFOPT_ENOMEM = -2
+DIFFOPT_EHIP = -3
+
+
+class DiffoptError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__("diffopt error %d: %s" % (code, message))
+        self.code = code
+
+
+def _load_library():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(
+            "libdiffopt.so is not built (%s); run `python -m paper_2211_06934_amd.build`" % _LIB_PATH)
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i64, i32, f64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double
+    pp = ctypes.POINTER(ctypes.c_void_p)
+    p64 = ctypes.POINTER(ctypes.c_int64)
+    hyper = [i64, f64, f64, f64, f64, f64]  # count, lr, b1, b2, eps, eps_root
+    sig = {
+        "diffopt_last_error": (ctypes.c_char_p, []),
+        "diffopt_segtable_create": (ctypes.c_int, [i64, p64, p64, i32, ctypes.POINTER(vp)]),
+        "diffopt_segtable_destroy": (None, [vp]),
+        "diffopt_segtable_total": (i64, [vp]),
+        "diffopt_segtable_nseg": (i64, [vp]),
+        "diffopt_tree_flatten": (ctypes.c_int, [vp, vp, vp, vp]),
+        "diffopt_tree_unflatten": (ctypes.c_int, [vp, vp, vp, vp]),
+        "diffopt_adam_fwd": (ctypes.c_int, [vp, vp, vp, vp, i64, *hyper, vp, vp, vp, vp, vp]),
+        "diffopt_adam_bwd": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, *hyper, vp, vp, vp, vp, vp]),
+        "diffopt_adam_unrolled_fwd": (ctypes.c_int, [i64, i64, vp, pp, pp, pp, vp, *hyper, vp]),
+        "diffopt_adam_unrolled_bwd": (ctypes.c_int, [i64, i64, vp, pp, pp, pp, pp, vp, vp, *hyper, vp]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load_library()
+LIBRARY_PATH = _LIB_PATH
+
+
+def last_error() -> str:
+    """diffopt_last_error(): message of the last failing call on this thread."""
+    return _lib.diffopt_last_error().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != DIFFOPT_OK:
+        raise DiffoptError(rc, last_error())
+
+
+def _addr(x, what: str, dtype=torch.float32, n: Optional[int] = None) -> Optional[int]:
+    """Device address of a tensor (checked) or a raw integer address."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if not isinstance(x, torch.Tensor):
+        raise TypeError("%s: expected a torch.Tensor or an int address" % what)
+    if not x.is_cuda:
+        raise ValueError("%s: tensor must live in device memory" % what)
+    if dtype is not None and x.dtype != dtype:
+        raise ValueError("%s: expected dtype %s, got %s" % (what, dtype, x.dtype))
+    if not x.is_contiguous():
+        raise ValueError("%s: tensor must be contiguous" % what)
+    if n is not None and x.numel() != n:
+        raise ValueError("%s: expected %d elements, got %d" % (what, n, x.numel()))
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _ptr_array(items, what, n):
+    arr = (ctypes.c_void_p * len(items))()
+    for i, t in enumerate(items):
+        arr[i] = _addr(t, "%s[%d]" % (what, i), n=n)
+    return arr
+
+
+class SegTable:
+    """Owner of a diffopt_segtable handle (freed on close() or collection)."""
+
+    def __init__(self, handle: int, numel: Sequence[int], offsets, elem_bytes: int):
+        self.handle = handle
+        self.numel = list(numel)
+        self.offsets = None if offsets is None else list(offsets)
+        self.elem_bytes = elem_bytes
+
+    @property
+    def total(self) -> int:
+        return segtable_total(self)
+
+    @property
+    def nseg(self) -> int:
+        return segtable_nseg(self)
+
+    def close(self) -> None:
+        if self.handle:
+            _lib.diffopt_segtable_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def segtable_create(numel: Sequence[int], offsets: Optional[Sequence[int]] = None,
+                    elem_bytes: int = 4) -> SegTable:
+    """diffopt_segtable_create on the current device."""
+    k = len(numel)
+    n_arr = (ctypes.c_int64 * max(k, 1))(*[int(x) for x in numel])
+    o_arr = None
+    if offsets is not None:
+        if len(offsets) != k:
+            raise ValueError("offsets must have one entry per leaf")
+        o_arr = (ctypes.c_int64 * max(k, 1))(*[int(x) for x in offsets])
+    h = ctypes.c_void_p()
+    _check(_lib.diffopt_segtable_create(k, n_arr, o_arr, int(elem_bytes), ctypes.byref(h)))
+    return SegTable(h.value, numel, offsets, elem_bytes)
+
+
+def segtable_destroy(table: SegTable) -> None:
+    table.close()
+
+
+def segtable_total(table: SegTable) -> int:
+    return int(_lib.diffopt_segtable_total(table.handle))
+
+
+def segtable_nseg(table: SegTable) -> int:
+    return int(_lib.diffopt_segtable_nseg(table.handle))
+
+
+def tree_flatten(table: SegTable, leaf_ptrs, flat, stream=None) -> None:
+    """diffopt_tree_flatten: leaf_ptrs is a device int64 tensor of leaf addresses."""
+    _check(_lib.diffopt_tree_flatten(table.handle, _addr(leaf_ptrs, "leaf_ptrs", torch.int64),
+                                     _addr(flat, "flat", None), _stream(stream)))
+
+
+def tree_unflatten(table: SegTable, flat, leaf_ptrs, stream=None) -> None:
+    """diffopt_tree_unflatten."""
+    _check(_lib.diffopt_tree_unflatten(table.handle, _addr(flat, "flat", None),
+                                       _addr(leaf_ptrs, "leaf_ptrs", torch.int64), _stream(stream)))
+
+
+def adam_fwd(params, grad, mu, nu, count, lr, b1, b2, eps, eps_root,
+             params_out, mu_out, nu_out, update_out=None, stream=None, n: Optional[int] = None) -> None:
+    """diffopt_adam_fwd; n defaults to params.numel()."""
+    if n is None:
+        n = params.numel()
+    _check(_lib.diffopt_adam_fwd(
+        _addr(params, "params", n=n), _addr(grad, "grad", n=n), _addr(mu, "mu", n=n), _addr(nu, "nu", n=n),
+        int(n), int(count), float(lr), float(b1), float(b2), float(eps), float(eps_root),
+        _addr(params_out, "params_out", n=n), _addr(mu_out, "mu_out", n=n), _addr(nu_out, "nu_out", n=n),
+        _addr(update_out, "update_out", n=n), _stream(stream)))
+
+
+def adam_bwd(dupdate, dmu, dnu, grad, mu, nu, count, lr, b1, b2, eps, eps_root,
+             dparams, dgrad, dmu_in, dnu_in, stream=None, n: Optional[int] = None) -> None:
+    """diffopt_adam_bwd; dmu/dnu/dparams may be None."""
+    if n is None:
+        n = dupdate.numel()
+    _check(_lib.diffopt_adam_bwd(
+        _addr(dupdate, "dupdate", n=n), _addr(dmu, "dmu", n=n), _addr(dnu, "dnu", n=n),
+        _addr(grad, "grad", n=n), _addr(mu, "mu", n=n), _addr(nu, "nu", n=n),
+        int(n), int(count), float(lr), float(b1), float(b2), float(eps), float(eps_root),
+        _addr(dparams, "dparams", n=n), _addr(dgrad, "dgrad", n=n), _addr(dmu_in, "dmu_in", n=n),
+        _addr(dnu_in, "dnu_in", n=n), _stream(stream)))
+
+
+def adam_unrolled_fwd(p0, grads, mu_traj, nu_traj, pK, count0, lr, b1, b2, eps, eps_root,
+                      stream=None) -> None:
+    """diffopt_adam_unrolled_fwd; grads has K entries, mu_traj/nu_traj K+1."""
+    K = len(grads)
+    n = p0.numel()
+    if len(mu_traj) != K + 1 or len(nu_traj) != K + 1:
+        raise ValueError("mu_traj and nu_traj need K+1 entries")
+    _check(_lib.diffopt_adam_unrolled_fwd(
+        K, n, _addr(p0, "p0", n=n), _ptr_array(grads, "grads", n), _ptr_array(mu_traj, "mu_traj", n),
+        _ptr_array(nu_traj, "nu_traj", n), _addr(pK, "pK", n=n), int(count0), float(lr), float(b1),
+        float(b2), float(eps), float(eps_root), _stream(stream)))
+
+
+def adam_unrolled_bwd(dpK, grads, mu_traj, nu_traj, dgrads, dmu0, dnu0, count0, lr, b1, b2, eps,
+                      eps_root, stream=None) -> None:
+    """diffopt_adam_unrolled_bwd; mu_traj/nu_traj may hold K or K+1 entries."""
+    K = len(grads)
+    n = dpK.numel()
+    if len(dgrads) != K or len(mu_traj) < K or len(nu_traj) < K:
+        raise ValueError("dgrads needs K entries, mu_traj/nu_traj at least K")
+    _check(_lib.diffopt_adam_unrolled_bwd(
+        K, n, _addr(dpK, "dpK", n=n), _ptr_array(grads, "grads", n), _ptr_array(mu_traj[:K], "mu_traj", n),
+        _ptr_array(nu_traj[:K], "nu_traj", n), _ptr_array(dgrads, "dgrads", n), _addr(dmu0, "dmu0", n=n),
+        _addr(dnu0, "dnu0", n=n), int(count0), float(lr), float(b1), float(b2), float(eps), float(eps_root),
+        _stream(stream)))

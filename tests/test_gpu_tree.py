@@ -1,0 +1,183 @@
+"""GPU parity of tree flatten / unflatten (pack / unpack) against the oracle.
+
+Bit-exact for every element size (1, 2, 4, 8 bytes), for dense and gapped
+layouts, for leaves whose addresses are out of phase with their flat offsets,
+for windows of many tiny leaves (the LDS window bound), empty leaves, special
+fp32 bit patterns, and the full 20,000-leaf workload.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.support import assert_bits_equal
+from workloads import many_small, random_bits, random_shapes, special_f32
+
+pytestmark = pytest.mark.gpu
+
+DT = {1: (np.uint8, torch.uint8), 2: (np.float16, torch.float16), 4: (np.float32, torch.float32),
+      8: (np.float64, torch.float64)}
+
+
+def _np_to_dev(a, tdt):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda").view(tdt)
+
+
+def _ptrs(leaves):
+    return torch.tensor([x.data_ptr() for x in leaves], dtype=torch.int64).cuda()
+
+
+def _make_leaves(host_leaves, tdt, mode, seed):
+    """Device copies of host leaves: separate allocations, or views at random
+    element offsets inside one big buffer (arbitrary 16-byte phases)."""
+    if mode == "separate":
+        return [_np_to_dev(x.reshape(-1), tdt) if x.size else torch.empty(0, dtype=tdt, device="cuda")
+                for x in host_leaves]
+    rng = np.random.default_rng(seed)
+    total = sum(x.size for x in host_leaves) + 16 * (len(host_leaves) + 1)
+    big = torch.zeros(total, dtype=tdt, device="cuda")
+    out = []
+    pos = int(rng.integers(0, 8))
+    for x in host_leaves:
+        view = big[pos:pos + x.size]
+        if x.size:
+            view.copy_(_np_to_dev(x.reshape(-1), tdt))
+        out.append(view)
+        pos += x.size + int(rng.integers(0, 9))
+    return out
+
+
+def _roundtrip(host_leaves, eb, mode, seed, offsets=None):
+    import paper_2211_06934_amd as P
+    ndt, tdt = DT[eb]
+    numel = [x.size for x in host_leaves]
+    table = P.segtable_create(numel, offsets, eb)
+    n = table.total
+    leaves = _make_leaves(host_leaves, tdt, mode, seed)
+    fill = random_bits(max(n, 1), ndt, seed + 7)[:n]
+    flat = _np_to_dev(fill, tdt)  # gaps must keep these bits
+    P.tree_flatten(table, _ptrs(leaves), flat)
+    torch.cuda.synchronize()
+    expect = np.array(fill, copy=True)
+    ref = oracle.pack([x.reshape(-1) for x in host_leaves], flat_len=n, offsets=offsets, dtype=ndt)
+    if offsets is None:
+        expect = ref
+    else:
+        for o, x in zip(offsets, host_leaves):
+            expect[o:o + x.size] = x.reshape(-1)
+        covered = np.zeros(n, bool)
+        for o, x in zip(offsets, host_leaves):
+            covered[o:o + x.size] = True
+        assert_bits_equal(ref[covered], expect[covered], "oracle")
+    got = flat.cpu().numpy().view(ndt)
+    assert_bits_equal(got, expect, "flatten")
+
+    # unflatten into fresh leaves of the same layout mode, compare with the oracle
+    outs = _make_leaves([np.zeros_like(x) for x in host_leaves], tdt, mode, seed + 1)
+    P.tree_unflatten(table, flat, _ptrs(outs))
+    torch.cuda.synchronize()
+    ref_leaves = oracle.unpack(expect, [x.shape for x in host_leaves], offsets=offsets)
+    for i, (o, r) in enumerate(zip(outs, ref_leaves)):
+        assert_bits_equal(o.cpu().numpy().view(ndt).reshape(-1), r.reshape(-1), "unflatten leaf %d" % i)
+    table.close()
+
+
+@pytest.mark.parametrize("eb", [4, 1, 2, 8])
+@pytest.mark.parametrize("mode", ["separate", "packed-views"])
+def test_random_trees_bit_exact(eb, mode):
+    shapes = random_shapes(400, 3000, seed=eb)
+    ndt = DT[eb][0]
+    leaves = [random_bits(int(np.prod(s)), ndt, seed=100 * eb + i).reshape(s) for i, s in enumerate(shapes)]
+    _roundtrip(leaves, eb, mode, seed=eb)
+
+
+@pytest.mark.parametrize("eb", [4, 2])
+def test_explicit_offsets_with_gaps(eb):
+    rng = np.random.default_rng(3)
+    ndt = DT[eb][0]
+    leaves = [random_bits(int(k), ndt, seed=int(k) + i) for i, k in
+              enumerate(rng.integers(0, 3000, size=120))]
+    order = rng.permutation(len(leaves))  # table order differs from flat order
+    offsets = [0] * len(leaves)
+    pos = int(rng.integers(0, 5))
+    for j in order:
+        offsets[j] = pos
+        pos += leaves[j].size + int(rng.integers(0, 7))
+    _roundtrip(leaves, eb, "packed-views", seed=11, offsets=offsets)
+
+
+def test_special_values_survive():
+    sp = special_f32()
+    leaves = [np.tile(sp, k)[: (k * 5) % 41 + 1] for k in range(1, 60)]
+    _roundtrip(leaves, 4, "packed-views", seed=5)
+    _roundtrip(leaves, 4, "separate", seed=6)
+
+
+@pytest.mark.parametrize("size", [1, 2, 3, 5])
+def test_window_of_tiny_leaves(size):
+    # 20,000 tiny leaves: every tile holds the largest window of leaves the
+    # LDS staging allows, plus empty leaves sprinkled between them.
+    shapes = []
+    for i in range(20000):
+        shapes.append((0,) if i % 13 == 0 else (size + (i % 3 == 0),))
+    leaves = [random_bits(int(np.prod(s)), np.float32, seed=i % 1000).reshape(s) for i, s in enumerate(shapes)]
+    _roundtrip(leaves, 4, "separate" if size % 2 else "packed-views", seed=size)
+
+
+def test_edge_tables():
+    import paper_2211_06934_amd as P
+    # no leaves, all-empty leaves: no-ops with total 0
+    for numel in ([], [0, 0, 0]):
+        t = P.segtable_create(numel)
+        assert t.total == 0 and t.nseg == len(numel)
+        f = torch.empty(0, dtype=torch.float32, device="cuda")
+        P.tree_flatten(t, torch.zeros(max(len(numel), 1), dtype=torch.int64, device="cuda"), f)
+        P.tree_unflatten(t, f, torch.zeros(max(len(numel), 1), dtype=torch.int64, device="cuda"))
+    # a single leaf is a plain copy, odd length, both layouts
+    x = random_bits(1_000_003, np.float32, seed=1)
+    _roundtrip([x], 4, "separate", seed=1)
+    _roundtrip([x], 4, "packed-views", seed=2)
+    # overlap is rejected
+    with pytest.raises(P.DiffoptError):
+        P.segtable_create([4, 4], [0, 3])
+    torch.cuda.synchronize()
+
+
+def test_python_tree_api_roundtrip():
+    import paper_2211_06934_amd as P
+    torch.manual_seed(0)
+    tree = {"b": [torch.randn(3, 5, device="cuda"), torch.randn(7, device="cuda")],
+            "a": (torch.randn(1, device="cuda"), {"z": torch.randn(2, 2, 2, device="cuda"), "y": None}),
+            "c": torch.randn(0, device="cuda")}
+    flat, spec = P.tree.flatten(tree)
+    leaves, _ = P.tree.tree_leaves(tree)
+    assert torch.equal(flat, torch.cat([x.reshape(-1) for x in leaves]))
+    back = P.tree.unflatten(flat, spec)
+    assert torch.equal(back["b"][0], tree["b"][0]) and torch.equal(back["a"][1]["z"], tree["a"][1]["z"])
+    assert back["a"][1]["y"] is None and isinstance(back["a"], tuple)
+
+
+def test_many_small_full_size_bit_exact():
+    # The 20,000-leaf workload at full size: flatten separately allocated leaves,
+    # compare the whole flat buffer with the oracle's pack, then unflatten.
+    import paper_2211_06934_amd as P
+    w = many_small()
+    numel = w.numels
+    n = w.n
+    src = torch.empty(n, dtype=torch.float32, device="cuda")
+    src.view(torch.int32).random_(generator=torch.Generator(device="cuda").manual_seed(9))
+    leaves = list(torch.split(src.clone(), numel))
+    leaves = [x.clone() for x in leaves]  # separate allocations
+    table = P.segtable_create(numel)
+    assert table.total == n
+    flat = torch.empty(n, dtype=torch.float32, device="cuda")
+    P.tree_flatten(table, _ptrs(leaves), flat)
+    torch.cuda.synchronize()
+    host_leaves = [x.cpu().numpy() for x in leaves]
+    ref = oracle.pack(host_leaves)
+    assert_bits_equal(flat.cpu().numpy(), ref, "flatten 20k")
+    outs = [torch.empty_like(x) for x in leaves]
+    P.tree_unflatten(table, flat, _ptrs(outs))
+    torch.cuda.synchronize()
+    got = torch.cat(outs).cpu().numpy()
+    assert_bits_equal(got, np.concatenate(host_leaves), "unflatten 20k")
