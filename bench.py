@@ -79,18 +79,23 @@ def setup_many_small(torch, P, w):
     K, n, numel = w.K, w.n, w.numels
     dev = "cuda"
 
-    def tree_from(flat):  # separately allocated leaves holding flat's values
-        return [x.clone() for x in torch.split(flat, numel)]
-
     def ptrs(leaves):
         return torch.tensor([x.data_ptr() for x in leaves], dtype=torch.int64).to(dev)
+
+    table = P.segtable_create(numel)
+    assert table.total == n
+
+    def tree_from(flat):
+        # separately allocated leaves (one allocation each, as a module's
+        # parameters are), filled from `flat` by one unflatten launch
+        leaves = [torch.empty(k, dtype=torch.float32, device=dev) for k in numel]
+        P.tree_unflatten(table, flat, ptrs(leaves))
+        return leaves
 
     p_tree = tree_from(torch_normal(n, 0.05, 101, dev))
     g_trees = [tree_from(torch_normal(n, w.grad_std, 110 + k, dev)) for k in range(K)]
     pK_tree = [torch.empty_like(x) for x in p_tree]
     dg_trees = [[torch.empty_like(x) for x in p_tree] for _ in range(K)]
-    table = P.segtable_create(numel)
-    assert table.total == n
     z = lambda: torch.zeros(n, dtype=torch.float32, device=dev)  # noqa: E731
     e = lambda: torch.empty(n, dtype=torch.float32, device=dev)  # noqa: E731
     S = dict(
