@@ -13,11 +13,18 @@
 
 #include "common.hpp"
 
+// Launch shape, chosen by measurement on MI355X (fp32, n ~ 1.2e8):
+// 1024-thread workgroups, one 16-byte vector per thread per array.  Smaller
+// workgroups with more vectors per thread, and persistent grid-stride grids of
+// 8-32 waves per CU, measured 1-20% slower.
 #ifndef DIFFOPT_FWD_U
-#define DIFFOPT_FWD_U 4  // 16-byte vectors per thread per array, forward
+#define DIFFOPT_FWD_U 1  // 16-byte vectors per thread per array, forward
 #endif
 #ifndef DIFFOPT_BWD_U
-#define DIFFOPT_BWD_U 2  // 16-byte vectors per thread per array, backward
+#define DIFFOPT_BWD_U 1  // 16-byte vectors per thread per array, backward
+#endif
+#ifndef DIFFOPT_ADAM_BLOCK
+#define DIFFOPT_ADAM_BLOCK 1024  // threads per workgroup of the Adam kernels
 #endif
 #ifndef DIFFOPT_NT_LOADS
 #define DIFFOPT_NT_LOADS 1  // streaming (non-temporal) loads of the inputs
@@ -158,21 +165,25 @@ __device__ __forceinline__ BwdOut bwd_elem(float dP, float dM, float dV, float g
 }
 
 // ---- kernels -----------------------------------------------------------------
-// Vector kernels: block b covers 16-byte vectors [b*256*U, (b+1)*256*U); lane
-// t of the block takes vectors t, t+256, ... so each load instruction of a
-// wave is one contiguous 1 KiB.  The last block also finishes the n % 4 tail.
+// Vector kernels: tile t covers 16-byte vectors [t*B*U, (t+1)*B*U) for B
+// threads per workgroup; lane j of the workgroup takes vectors j, j+B, ... so
+// each load instruction of a wave is one contiguous 1 KiB.  Workgroups walk
+// tiles with a grid stride (one tile each when the grid covers them all).
+// Full tiles skip the per-vector bounds checks.  The last workgroup also
+// finishes the n % 4 tail element by element.
 
-template <int U, bool WU>
-__global__ __launch_bounds__(kBlock) void adam_fwd_vec(const float* p, const float* g, const float* m,
-                                                       const float* v, float* po, float* mo, float* vo,
-                                                       float* uo, int64_t n, AdamCoef c) {
-  const int64_t nv = n >> 2;
-  const int64_t base = (int64_t)blockIdx.x * (kBlock * U) + threadIdx.x;
+constexpr int kAB = DIFFOPT_ADAM_BLOCK;
+
+template <int U, bool WU, bool GUARD>
+__device__ __forceinline__ void fwd_tile(int64_t t, int64_t nv, const float* p, const float* g, const float* m,
+                                         const float* v, float* po, float* mo, float* vo, float* uo,
+                                         const AdamCoef& c) {
+  const int64_t base = t * (kAB * U) + threadIdx.x;
   f32x4 P[U], G[U], M[U], V[U];
 #pragma unroll
   for (int k = 0; k < U; ++k) {
-    const int64_t i = base + (int64_t)k * kBlock;
-    if (i < nv) {
+    const int64_t i = base + (int64_t)k * kAB;
+    if (!GUARD || i < nv) {
       P[k] = ld(reinterpret_cast<const f32x4*>(p) + i);
       G[k] = ld(reinterpret_cast<const f32x4*>(g) + i);
       M[k] = ld(reinterpret_cast<const f32x4*>(m) + i);
@@ -181,8 +192,8 @@ __global__ __launch_bounds__(kBlock) void adam_fwd_vec(const float* p, const flo
   }
 #pragma unroll
   for (int k = 0; k < U; ++k) {
-    const int64_t i = base + (int64_t)k * kBlock;
-    if (i < nv) {
+    const int64_t i = base + (int64_t)k * kAB;
+    if (!GUARD || i < nv) {
       f32x4 rp, rm, rv, ru;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -198,6 +209,19 @@ __global__ __launch_bounds__(kBlock) void adam_fwd_vec(const float* p, const flo
       if (WU) st(reinterpret_cast<f32x4*>(uo) + i, ru);
     }
   }
+}
+
+template <int U, bool WU>
+__global__ __launch_bounds__(kAB) void adam_fwd_vec(const float* p, const float* g, const float* m,
+                                                    const float* v, float* po, float* mo, float* vo, float* uo,
+                                                    int64_t n, AdamCoef c) {
+  const int64_t nv = n >> 2;
+  const int64_t nfull = nv / (kAB * U);
+  const int64_t ntiles = (nv + kAB * U - 1) / (kAB * U);
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    if (t < nfull) fwd_tile<U, WU, false>(t, nv, p, g, m, v, po, mo, vo, uo, c);
+    else fwd_tile<U, WU, true>(t, nv, p, g, m, v, po, mo, vo, uo, c);
+  }
   if (blockIdx.x == gridDim.x - 1) {
     const int64_t e = (nv << 2) + threadIdx.x;
     if (e < n) {
@@ -212,13 +236,13 @@ __global__ __launch_bounds__(kBlock) void adam_fwd_vec(const float* p, const flo
 
 // Scalar kernel for pointers that are not 16-byte aligned.
 template <bool WU>
-__global__ __launch_bounds__(kBlock) void adam_fwd_scalar(const float* p, const float* g, const float* m,
-                                                          const float* v, float* po, float* mo, float* vo,
-                                                          float* uo, int64_t n, AdamCoef c) {
-  const int64_t base = (int64_t)blockIdx.x * (kBlock * 4) + threadIdx.x;
+__global__ __launch_bounds__(kAB) void adam_fwd_scalar(const float* p, const float* g, const float* m,
+                                                       const float* v, float* po, float* mo, float* vo, float* uo,
+                                                       int64_t n, AdamCoef c) {
+  const int64_t base = (int64_t)blockIdx.x * (kAB * 4) + threadIdx.x;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const int64_t e = base + (int64_t)k * kBlock;
+    const int64_t e = base + (int64_t)k * kAB;
     if (e < n) {
       const FwdOut o = fwd_elem(p[e], g[e], m[e], v[e], c);
       po[e] = o.p;
@@ -229,18 +253,16 @@ __global__ __launch_bounds__(kBlock) void adam_fwd_scalar(const float* p, const 
   }
 }
 
-template <int U, bool HAS_MV, bool WDP>
-__global__ __launch_bounds__(kBlock) void adam_bwd_vec(const float* dP, const float* dM, const float* dV,
-                                                       const float* g, const float* m, const float* v,
-                                                       float* dpo, float* dgo, float* dmo, float* dvo,
-                                                       int64_t n, AdamCoef c) {
-  const int64_t nv = n >> 2;
-  const int64_t base = (int64_t)blockIdx.x * (kBlock * U) + threadIdx.x;
+template <int U, bool HAS_MV, bool WDP, bool GUARD>
+__device__ __forceinline__ void bwd_tile(int64_t t, int64_t nv, const float* dP, const float* dM,
+                                         const float* dV, const float* g, const float* m, const float* v,
+                                         float* dpo, float* dgo, float* dmo, float* dvo, const AdamCoef& c) {
+  const int64_t base = t * (kAB * U) + threadIdx.x;
   f32x4 P[U], Mb[U], Vb[U], G[U], M[U], V[U];
 #pragma unroll
   for (int k = 0; k < U; ++k) {
-    const int64_t i = base + (int64_t)k * kBlock;
-    if (i < nv) {
+    const int64_t i = base + (int64_t)k * kAB;
+    if (!GUARD || i < nv) {
       P[k] = ld(reinterpret_cast<const f32x4*>(dP) + i);
       if (HAS_MV) {
         Mb[k] = ld(reinterpret_cast<const f32x4*>(dM) + i);
@@ -253,13 +275,13 @@ __global__ __launch_bounds__(kBlock) void adam_bwd_vec(const float* dP, const fl
   }
 #pragma unroll
   for (int k = 0; k < U; ++k) {
-    const int64_t i = base + (int64_t)k * kBlock;
-    if (i < nv) {
+    const int64_t i = base + (int64_t)k * kAB;
+    if (!GUARD || i < nv) {
       f32x4 rg, rm, rv;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const BwdOut o = bwd_elem<HAS_MV>(P[k][e], HAS_MV ? Mb[k][e] : 0.0f, HAS_MV ? Vb[k][e] : 0.0f,
-                                          G[k][e], M[k][e], V[k][e], c);
+        const BwdOut o = bwd_elem<HAS_MV>(P[k][e], HAS_MV ? Mb[k][e] : 0.0f, HAS_MV ? Vb[k][e] : 0.0f, G[k][e],
+                                          M[k][e], V[k][e], c);
         rg[e] = o.g;
         rm[e] = o.m;
         rv[e] = o.v;
@@ -270,11 +292,23 @@ __global__ __launch_bounds__(kBlock) void adam_bwd_vec(const float* dP, const fl
       if (WDP) st(reinterpret_cast<f32x4*>(dpo) + i, P[k]);
     }
   }
+}
+
+template <int U, bool HAS_MV, bool WDP>
+__global__ __launch_bounds__(kAB) void adam_bwd_vec(const float* dP, const float* dM, const float* dV,
+                                                    const float* g, const float* m, const float* v, float* dpo,
+                                                    float* dgo, float* dmo, float* dvo, int64_t n, AdamCoef c) {
+  const int64_t nv = n >> 2;
+  const int64_t nfull = nv / (kAB * U);
+  const int64_t ntiles = (nv + kAB * U - 1) / (kAB * U);
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    if (t < nfull) bwd_tile<U, HAS_MV, WDP, false>(t, nv, dP, dM, dV, g, m, v, dpo, dgo, dmo, dvo, c);
+    else bwd_tile<U, HAS_MV, WDP, true>(t, nv, dP, dM, dV, g, m, v, dpo, dgo, dmo, dvo, c);
+  }
   if (blockIdx.x == gridDim.x - 1) {
     const int64_t e = (nv << 2) + threadIdx.x;
     if (e < n) {
-      const BwdOut o = bwd_elem<HAS_MV>(dP[e], HAS_MV ? dM[e] : 0.0f, HAS_MV ? dV[e] : 0.0f, g[e], m[e],
-                                        v[e], c);
+      const BwdOut o = bwd_elem<HAS_MV>(dP[e], HAS_MV ? dM[e] : 0.0f, HAS_MV ? dV[e] : 0.0f, g[e], m[e], v[e], c);
       dgo[e] = o.g;
       dmo[e] = o.m;
       dvo[e] = o.v;
@@ -284,17 +318,15 @@ __global__ __launch_bounds__(kBlock) void adam_bwd_vec(const float* dP, const fl
 }
 
 template <bool HAS_MV, bool WDP>
-__global__ __launch_bounds__(kBlock) void adam_bwd_scalar(const float* dP, const float* dM, const float* dV,
-                                                          const float* g, const float* m, const float* v,
-                                                          float* dpo, float* dgo, float* dmo, float* dvo,
-                                                          int64_t n, AdamCoef c) {
-  const int64_t base = (int64_t)blockIdx.x * (kBlock * 4) + threadIdx.x;
+__global__ __launch_bounds__(kAB) void adam_bwd_scalar(const float* dP, const float* dM, const float* dV,
+                                                       const float* g, const float* m, const float* v, float* dpo,
+                                                       float* dgo, float* dmo, float* dvo, int64_t n, AdamCoef c) {
+  const int64_t base = (int64_t)blockIdx.x * (kAB * 4) + threadIdx.x;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const int64_t e = base + (int64_t)k * kBlock;
+    const int64_t e = base + (int64_t)k * kAB;
     if (e < n) {
-      const BwdOut o = bwd_elem<HAS_MV>(dP[e], HAS_MV ? dM[e] : 0.0f, HAS_MV ? dV[e] : 0.0f, g[e], m[e],
-                                        v[e], c);
+      const BwdOut o = bwd_elem<HAS_MV>(dP[e], HAS_MV ? dM[e] : 0.0f, HAS_MV ? dV[e] : 0.0f, g[e], m[e], v[e], c);
       dgo[e] = o.g;
       dmo[e] = o.m;
       dvo[e] = o.v;
@@ -308,6 +340,13 @@ __global__ __launch_bounds__(kBlock) void adam_bwd_scalar(const float* dP, const
 inline bool aligned16(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline bool aligned4(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
+// One workgroup per tile; the kernels' grid-stride loop covers the (never
+// reached in practice) case of more tiles than a grid dimension holds.
+int64_t grid_for(int64_t tiles) {
+  if (tiles < 1) return 1;
+  return tiles < 0x7fffffff ? tiles : 0x7fffffff;
+}
+
 int launch_fwd(const float* p, const float* g, const float* m, const float* v, int64_t n, const AdamCoef& c,
                float* po, float* mo, float* vo, float* uo, hipStream_t st) {
   if (n == 0) return DIFFOPT_OK;
@@ -315,22 +354,21 @@ int launch_fwd(const float* p, const float* g, const float* m, const float* v, i
                    aligned16(mo) && aligned16(vo) && aligned16(uo);
   if (vec) {
     constexpr int U = DIFFOPT_FWD_U;
-    const int64_t nv = n >> 2;
-    const int64_t blocks = nv > 0 ? (nv + kBlock * U - 1) / (kBlock * U) : 1;
+    const int64_t blocks = grid_for(((n >> 2) + kAB * U - 1) / (kAB * U));
     if (uo)
-      hipLaunchKernelGGL((adam_fwd_vec<U, true>), dim3((unsigned)blocks), dim3(kBlock), 0, st, p, g, m, v, po,
-                         mo, vo, uo, n, c);
+      hipLaunchKernelGGL((adam_fwd_vec<U, true>), dim3((unsigned)blocks), dim3(kAB), 0, st, p, g, m, v, po, mo, vo,
+                         uo, n, c);
     else
-      hipLaunchKernelGGL((adam_fwd_vec<U, false>), dim3((unsigned)blocks), dim3(kBlock), 0, st, p, g, m, v, po,
-                         mo, vo, uo, n, c);
+      hipLaunchKernelGGL((adam_fwd_vec<U, false>), dim3((unsigned)blocks), dim3(kAB), 0, st, p, g, m, v, po, mo,
+                         vo, uo, n, c);
   } else {
-    const int64_t blocks = (n + kBlock * 4 - 1) / (kBlock * 4);
+    const int64_t blocks = (n + kAB * 4 - 1) / (kAB * 4);
     if (uo)
-      hipLaunchKernelGGL((adam_fwd_scalar<true>), dim3((unsigned)blocks), dim3(kBlock), 0, st, p, g, m, v, po,
-                         mo, vo, uo, n, c);
+      hipLaunchKernelGGL((adam_fwd_scalar<true>), dim3((unsigned)blocks), dim3(kAB), 0, st, p, g, m, v, po, mo, vo,
+                         uo, n, c);
     else
-      hipLaunchKernelGGL((adam_fwd_scalar<false>), dim3((unsigned)blocks), dim3(kBlock), 0, st, p, g, m, v, po,
-                         mo, vo, uo, n, c);
+      hipLaunchKernelGGL((adam_fwd_scalar<false>), dim3((unsigned)blocks), dim3(kAB), 0, st, p, g, m, v, po, mo,
+                         vo, uo, n, c);
   }
   return launch_status("diffopt_adam_fwd");
 }
@@ -341,14 +379,13 @@ void launch_bwd_t(bool vec, const float* dP, const float* dM, const float* dV, c
                   hipStream_t st) {
   if (vec) {
     constexpr int U = DIFFOPT_BWD_U;
-    const int64_t nv = n >> 2;
-    const int64_t blocks = nv > 0 ? (nv + kBlock * U - 1) / (kBlock * U) : 1;
-    hipLaunchKernelGGL((adam_bwd_vec<U, HAS_MV, WDP>), dim3((unsigned)blocks), dim3(kBlock), 0, st, dP, dM, dV,
-                       g, m, v, dpo, dgo, dmo, dvo, n, c);
+    const int64_t blocks = grid_for(((n >> 2) + kAB * U - 1) / (kAB * U));
+    hipLaunchKernelGGL((adam_bwd_vec<U, HAS_MV, WDP>), dim3((unsigned)blocks), dim3(kAB), 0, st, dP, dM, dV, g, m,
+                       v, dpo, dgo, dmo, dvo, n, c);
   } else {
-    const int64_t blocks = (n + kBlock * 4 - 1) / (kBlock * 4);
-    hipLaunchKernelGGL((adam_bwd_scalar<HAS_MV, WDP>), dim3((unsigned)blocks), dim3(kBlock), 0, st, dP, dM, dV,
-                       g, m, v, dpo, dgo, dmo, dvo, n, c);
+    const int64_t blocks = (n + kAB * 4 - 1) / (kAB * 4);
+    hipLaunchKernelGGL((adam_bwd_scalar<HAS_MV, WDP>), dim3((unsigned)blocks), dim3(kAB), 0, st, dP, dM, dV, g, m,
+                       v, dpo, dgo, dmo, dvo, n, c);
   }
 }
 
