@@ -7,6 +7,10 @@ One step = one pass of the whole path over one batch of synthetic input:
   -> tree unflatten of p_K and of the K gradient cotangents.
 Default workload: the many-small-tensor tree (20,000 fp32 leaves, log-uniform
 sizes in [1, 65536], K = 3).  All inputs are resident in HBM before timing.
+Other trees (--workload tiny_mlp | convnet32 | resnet18_k1 | resnet18_k10)
+run the same step; --workload flat_1b times one interior fwd + bwd step on a
+single 10^9-element buffer; --graph replays one captured step as a HIP graph
+(the small trees are launch-bound).
 
 Prints ONE JSON line.  `value` is Adam fwd+bwd parameter-steps per second for
 the whole pass (n * K / step time); `roofline` covers the dominant kernel
@@ -43,7 +47,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="many_small", choices=["many_small", "flat_1b"])
+    ap.add_argument("--workload", default="many_small",
+                    choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10"])
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step in a HIP graph and time replays (no per-phase split)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     return ap.parse_args()
@@ -74,7 +81,7 @@ def traffic_from_profile(kernel, workload):
 # --------------------------------------------------------------------- setup
 
 
-def setup_many_small(torch, P, w):
+def setup_tree(torch, P, w):
     from workloads import HYPER, torch_normal
     K, n, numel = w.K, w.n, w.numels
     dev = "cuda"
@@ -110,7 +117,7 @@ def setup_many_small(torch, P, w):
     return S
 
 
-def step_many_small(P, S, ev=None):
+def step_tree(P, S, ev=None):
     """One pass; if ev is given, records ev[0..4] around the four phases."""
     h = S["hyper"]
     args = (S["count0"], h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
@@ -134,7 +141,7 @@ def step_many_small(P, S, ev=None):
         ev[4].record()
 
 
-def phases_many_small(S):
+def phases_tree(S):
     """(name, kernel, launches per step, algorithmic bytes per step) per phase."""
     K, n = S["K"], S["n"]
     return [
@@ -179,7 +186,7 @@ def phases_flat_1b(S):
 # ------------------------------------------------------------- CPU baseline
 
 
-def cpu_baseline_many_small(w, target_s):
+def cpu_baseline_tree(w, target_s):
     """Time the CPU oracle (single thread) on the first leaves of the tree: pack
     p and K grads, K-step fwd, K-step bwd, unpack p_K and K cotangents."""
     import numpy as np
@@ -218,7 +225,7 @@ def cpu_baseline_many_small(w, target_s):
         return n, (t1 - t0) + (t3 - t2) + (t4 - t3)
 
     # calibrate on a small prefix, then size the sample to about target_s
-    n_small, t_small = run(200)
+    n_small, t_small = run(min(200, len(numel)))
     rate = n_small / max(t_small, 1e-9)
     want = rate * target_s
     acc, nleaves = 0, 0
@@ -277,10 +284,10 @@ def main():
         sys.stderr.write("bench.py: no GPU visible\n")
         sys.exit(1)
     w = WORKLOADS[a.workload]()
-    if a.workload == "many_small":
-        S, step, phases = setup_many_small(torch, P, w), step_many_small, phases_many_small
-    else:
+    if a.workload == "flat_1b":
         S, step, phases = setup_flat_1b(torch, P, w), step_flat_1b, phases_flat_1b
+    else:
+        S, step, phases = setup_tree(torch, P, w), step_tree, phases_tree
     ph = phases(S)
     nph = len(ph)
     torch.cuda.synchronize()
@@ -297,41 +304,61 @@ def main():
         step(P, S)
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)] for _ in range(a.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record()
-    for s in range(a.steps):
-        step(P, S, evs[s])
-    t_end.record()
-    torch.cuda.synchronize()
+    phase_ms = None
+    if a.graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step(P, S)
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(P, S)
+        graph.replay()
+        torch.cuda.synchronize()
+        t_start.record()
+        for s in range(a.steps):
+            graph.replay()
+        t_end.record()
+        torch.cuda.synchronize()
+    else:
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)] for _ in range(a.steps)]
+        torch.cuda.synchronize()
+        t_start.record()
+        for s in range(a.steps):
+            step(P, S, evs[s])
+        t_end.record()
+        torch.cuda.synchronize()
+        phase_ms = [sum(e[i].elapsed_time(e[i + 1]) for e in evs) / a.steps for i in range(nph)]
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / a.steps
-    phase_ms = [sum(e[i].elapsed_time(e[i + 1]) for e in evs) / a.steps for i in range(nph)]
 
     n, K = S["n"], S["K"]
     bytes_step = sum(p[3] for p in ph)
     value = n * K / (ms_step * 1e-3)
     gbs = bytes_step / (ms_step * 1e-3) / 1e9
-    breakdown = {}
-    for (name, kern, launches, byts), t in zip(ph, phase_ms):
-        breakdown[name] = {"ms": round(t, 4), "launches": launches, "GB/s": round(byts / (t * 1e-3) / 1e9, 1),
-                           "frac": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-    dom = max(range(nph), key=lambda i: phase_ms[i])
-    dname, dkern, dlaunch, dbytes = ph[dom]
-    avg_launch_s = phase_ms[dom] * 1e-3 / dlaunch
-    per_launch_bytes = dbytes / dlaunch
-    achieved = per_launch_bytes / avg_launch_s / 1e9
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic_from_profile(dkern, a.workload),
-                "kernel": dkern, "bytes_per_launch": int(per_launch_bytes),
-                "avg_launch_us": round(avg_launch_s * 1e6, 2)}
+    breakdown, roofline = {}, None
+    if phase_ms is not None:
+        for (name, kern, launches, byts), t in zip(ph, phase_ms):
+            breakdown[name] = {"ms": round(t, 4), "launches": launches,
+                               "GB/s": round(byts / (t * 1e-3) / 1e9, 1),
+                               "frac": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        dom = max(range(nph), key=lambda i: phase_ms[i])
+        dname, dkern, dlaunch, dbytes = ph[dom]
+        avg_launch_s = phase_ms[dom] * 1e-3 / dlaunch
+        per_launch_bytes = dbytes / dlaunch
+        achieved = per_launch_bytes / avg_launch_s / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": traffic_from_profile(dkern, a.workload),
+                    "kernel": dkern, "bytes_per_launch": int(per_launch_bytes),
+                    "avg_launch_us": round(avg_launch_s * 1e6, 2)}
 
     cpu = None
     if not a.no_cpu_baseline:
-        cpu = (cpu_baseline_many_small if a.workload == "many_small" else cpu_baseline_flat_1b)(w, a.cpu_seconds)
+        cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
         cpu["value"] = float("%.4g" % cpu["value"])
 
     out = {
@@ -339,9 +366,10 @@ def main():
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": w.description, "n_params": n, "leaves": w.nseg, "K": K,
-                   "step": "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg"
-                   if a.workload == "many_small" else "one Adam fwd + one Adam bwd (count 100, all cotangents)",
-                   "parallelism": "single GPU"},
+                   "step": "one Adam fwd + one Adam bwd (count 100, all cotangents)" if a.workload == "flat_1b"
+                   else "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg",
+                   "launch": "hip graph replay" if a.graph else "eager", "parallelism": "single GPU"},
+        "us_per_step": round(ms_step * 1e3, 2),
         "achieved_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
         "bytes_per_step": int(bytes_step), "phases": breakdown,
         "roofline": roofline, "cpu_baseline": cpu,

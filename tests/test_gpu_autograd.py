@@ -1,0 +1,144 @@
+"""GPU checks of the user-facing layers over the C ABI:
+
+- AdamFn (torch.autograd.Function around the fused step) inside a K-step
+  explicit-gradient loop, its meta-gradient via torch.autograd.grad against
+  the oracle's K-step backward;
+- capture of the unrolled forward + backward in a HIP graph (torch.cuda.graph),
+  replayed several times with eager work in between, every replay compared
+  with the eager result (the library allocates and synchronises nothing on
+  the path, so it is capture-safe).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.support import BWD_RTOL, FWD_RTOL, stats
+from workloads import HYPER, WORKLOADS, host_inputs
+
+pytestmark = pytest.mark.gpu
+
+LR, B1, B2, EPS = HYPER["lr"], HYPER["b1"], HYPER["b2"], HYPER["eps"]
+
+
+def test_adamfn_meta_gradient_matches_oracle():
+    import paper_2211_06934_amd as P
+    w = WORKLOADS["tiny_mlp"]()
+    K, n = w.K, w.n
+    inp = host_inputs(w)
+    opt = P.FlatAdam(lr=LR, b1=B1, b2=B2, eps=EPS, eps_root=0.0)
+    p0 = torch.from_numpy(inp.p0).cuda().requires_grad_()
+    grads = [torch.from_numpy(inp.grads[k]).cuda().requires_grad_() for k in range(K)]
+    state = opt.init(p0.detach())
+    p = p0
+    for k in range(K):
+        p, state = opt.step(p, grads[k], state)
+    assert state.count == K
+    cot = torch.from_numpy(inp.cot_p).cuda()
+    out = torch.autograd.grad((p * cot).sum(), [p0] + grads)
+    G = inp.grads.astype(np.float64)
+    z = np.zeros(n)
+    pK_ref, mt, vt = oracle.unrolled_fwd(inp.p0, G, z, z, 0, LR, B1, B2, EPS, 0.0)
+    _, dg_ref, _, _ = oracle.unrolled_bwd(inp.cot_p, G, mt, vt, 0, LR, B1, B2, EPS, 0.0)
+    assert stats(p.detach().cpu().numpy(), pK_ref)[1] < FWD_RTOL
+    assert np.array_equal(out[0].cpu().numpy(), inp.cot_p)  # identity params path
+    for k in range(K):
+        assert stats(out[1 + k].cpu().numpy(), dg_ref[k])[1] < BWD_RTOL, k
+
+
+def test_adamfn_moment_cotangents_flow():
+    # a loss that also reads the final moments: their cotangents enter the VJP
+    import paper_2211_06934_amd as P
+    n = 4099
+    rng = np.random.default_rng(3)
+    g = torch.tensor(rng.normal(0, 0.01, n), dtype=torch.float32, device="cuda", requires_grad=True)
+    m = torch.tensor(rng.normal(0, 1e-3, n), dtype=torch.float32, device="cuda", requires_grad=True)
+    v = torch.tensor(np.abs(rng.normal(0, 1e-4, n)), dtype=torch.float32, device="cuda", requires_grad=True)
+    p = torch.tensor(rng.normal(0, 0.05, n), dtype=torch.float32, device="cuda", requires_grad=True)
+    hyper = P.AdamHyper(LR, B1, B2, EPS, 1e-8)
+    po, mo, vo = P.AdamFn.apply(p, g, m, v, 9, hyper)
+    cP, cM, cV = (torch.tensor(rng.normal(0, 1, n), dtype=torch.float32, device="cuda") for _ in range(3))
+    out = torch.autograd.grad((po * cP).sum() + (mo * cM).sum() + (vo * cV).sum(), [p, g, m, v])
+    to = lambda t: t.detach().cpu().numpy().astype(np.float64)  # noqa: E731
+    ref = oracle.adam_bwd(to(cP), to(cM), to(cV), to(g), to(m), to(v), 9, LR, B1, B2, EPS, 1e-8)
+    mag = oracle.adam_bwd_mag(to(cP), to(cM), to(cV), to(g), to(m), to(v), 9, LR, B1, B2, EPS, 1e-8)
+    assert np.array_equal(to(out[0]), to(cP))
+    for got, r, mg in zip(out[1:], ref[1:], mag):
+        assert np.all(np.abs(to(got) - r) <= BWD_RTOL * mg)
+
+
+def test_unrolled_driver_in_hip_graph_replays():
+    import paper_2211_06934_amd as P
+    w = WORKLOADS["convnet32"]()
+    K, n = w.K, w.n
+    inp = host_inputs(w)
+    dev = "cuda"
+    p0 = torch.from_numpy(inp.p0).to(dev)
+    g = [torch.from_numpy(inp.grads[k]).to(dev) for k in range(K)]
+    mt = [torch.zeros(n, device=dev)] + [torch.empty(n, device=dev) for _ in range(K)]
+    vt = [torch.zeros(n, device=dev)] + [torch.empty(n, device=dev) for _ in range(K)]
+    pK = torch.empty(n, device=dev)
+    cot = torch.from_numpy(inp.cot_p).to(dev)
+    dg = [torch.empty(n, device=dev) for _ in range(K)]
+    dm0, dv0 = torch.empty(n, device=dev), torch.empty(n, device=dev)
+    args = (0, LR, B1, B2, EPS, 0.0)
+
+    def run():
+        P.adam_unrolled_fwd(p0, g, mt, vt, pK, *args)
+        P.adam_unrolled_bwd(cot, g, mt, vt, dg, dm0, dv0, *args)
+
+    run()
+    torch.cuda.synchronize()
+    eager = [x.clone() for x in [pK, dm0, dv0, *dg, *mt[1:], *vt[1:]]]
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        run()  # warm up on the capture stream
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    for rep in range(4):
+        for x in [pK, dm0, dv0, *dg, *mt[1:], *vt[1:]]:
+            x.fill_(float("nan"))  # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        now = [pK, dm0, dv0, *dg, *mt[1:], *vt[1:]]
+        for a, b in zip(now, eager):
+            assert torch.equal(a, b), rep
+
+
+def test_tree_flatten_in_hip_graph_replays():
+    import paper_2211_06934_amd as P
+    w = WORKLOADS["resnet18_k1"]()
+    numel = w.numels
+    leaves = [torch.randn(k, device="cuda") for k in numel]
+    ptrs = torch.tensor([x.data_ptr() for x in leaves], dtype=torch.int64, device="cuda")
+    table = P.segtable_create(numel)
+    flat = torch.empty(w.n, device="cuda")
+    outs = [torch.empty_like(x) for x in leaves]
+    optrs = torch.tensor([x.data_ptr() for x in outs], dtype=torch.int64, device="cuda")
+    ref = torch.cat(leaves)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        P.tree_flatten(table, ptrs, flat)
+        P.tree_unflatten(table, flat, optrs)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        P.tree_flatten(table, ptrs, flat)
+        P.tree_unflatten(table, flat, optrs)
+    for rep in range(3):
+        flat.zero_()
+        for o in outs:
+            o.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(flat, ref), rep
+        assert all(torch.equal(a, b) for a, b in zip(outs, leaves)), rep
