@@ -56,10 +56,18 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_source_sha():
+KERNEL_SOURCES = {  # the sources each kernel family is built from
+    "adam_fwd": ("adam.hip", "common.hpp"), "adam_bwd": ("adam.hip", "common.hpp"),
+    "tree_flatten": ("tree.hip", "common.hpp"), "tree_unflatten": ("tree.hip", "common.hpp"),
+}
+
+
+def kernel_source_sha(kernel=None):
+    """Hash of the HIP sources of one kernel family (all sources if None)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2211_06934_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    names = sorted(os.listdir(csrc)) if kernel is None else sorted(KERNEL_SOURCES[kernel])
+    for name in names:
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
@@ -73,7 +81,7 @@ def traffic_from_profile(kernel, workload):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_src_sha") != kernel_source_sha():
+    if rec.get("kernel_src_sha") != kernel_source_sha(kernel):
         return None
     return rec.get("bytes_per_launch")
 

@@ -61,7 +61,8 @@ const char* diffopt_last_error(void);
  */
 typedef struct diffopt_segtable diffopt_segtable;
 
-/* Build a table on the current HIP device.
+/* Build a table on the current HIP device (flatten/unflatten must run with
+ * that device current; any other device gives EINVAL).
  *   nseg        number of leaves S (>= 0)
  *   numel       host array [nseg], elements per leaf (>= 0; empty leaves ok)
  *   offsets     host array [nseg] of flat element offsets, or NULL for the

@@ -45,6 +45,9 @@
 #ifndef DIFFOPT_TREE_BLOCK
 #define DIFFOPT_TREE_BLOCK 256  // threads per workgroup of the copy kernel
 #endif
+#ifndef DIFFOPT_TREE_NT_LOADS
+#define DIFFOPT_TREE_NT_LOADS 0  // streaming loads of source vectors
+#endif
 #ifndef DIFFOPT_TREE_NT_STORES
 #define DIFFOPT_TREE_NT_STORES 1  // streaming stores of full destination vectors
 #endif
@@ -120,9 +123,9 @@ __device__ __forceinline__ u32x4 funnel(u32x4 w0, u32x4 w1, uint32_t s) {
 
 template <int E, bool PACK>
 __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restrict__ seg,
-                                                           const int64_t* __restrict__ tile_first,
-                                                           int64_t ngroups, const uint64_t* __restrict__ leaf_ptrs,
-                                                           uint64_t flat) {
+                                                        const int64_t* __restrict__ tile_first, int64_t ngroups,
+                                                        const uint64_t* __restrict__ leaf_ptrs, uint64_t flat,
+                                                        int dense_orig) {
   __shared__ int64_t s_goff[kWindowMax + 1];
   __shared__ int64_t s_fbase[kWindowMax];  // flat byte address of the leaf's range
   __shared__ int64_t s_bytes[kWindowMax];
@@ -132,53 +135,81 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
   const int64_t j0 = tile_first[b];
   const int W = (int)(tile_first[b + 1] - j0 + 1);
   for (int t = threadIdx.x; t <= W; t += kTB) {
+    // Without empty leaves the table index is the leaf index, so the leaf
+    // address is fetched alongside the table entry instead of after it.
+    const uint64_t lp = (dense_orig && t < W) ? leaf_ptrs[j0 + t] : 0;
     const SegEntry e = seg[j0 + t];
     s_goff[t] = e.goff;
     if (t < W) {
       s_fbase[t] = (int64_t)(flat + (uint64_t)(e.off * E));
       s_bytes[t] = e.numel * E;
-      s_leaf[t] = leaf_ptrs[e.orig];
+      s_leaf[t] = dense_orig ? lp : leaf_ptrs[e.orig];
     }
   }
   __syncthreads();
 
-  typedef typename ElemT<E>::T T;
+  // Phase 1 locates every group of this lane and issues all of its source
+  // loads; phase 2 stores.  Sources never overlap destinations, so all loads
+  // may go out before any store and each lane keeps kTreeU groups in flight.
+  u32x4 w0[kTreeU], w1[kTreeU];
+  uint64_t dst[kTreeU], lo_b[kTreeU], hi_b[kTreeU], delta[kTreeU];
+  uint32_t shift[kTreeU];
+  int kind[kTreeU];  // 0: nothing, 1: full aligned vector, 2: partial (element copy)
 #pragma unroll
   for (int u = 0; u < kTreeU; ++u) {
     const int64_t gidx = b * kTileGroups + (int64_t)u * kTB + threadIdx.x;
-    if (gidx >= ngroups) break;
-    // largest t with s_goff[t] <= gidx; s_goff[0] <= gidx holds by construction
-    int lo = 0, hi = W - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (s_goff[mid] <= gidx) lo = mid;
-      else hi = mid - 1;
-    }
-    const uint64_t k = (uint64_t)(gidx - s_goff[lo]);
-    const uint64_t fb = (uint64_t)s_fbase[lo];
-    const uint64_t lb = s_leaf[lo];
-    const uint64_t nb = (uint64_t)s_bytes[lo];
-    const uint64_t dst0 = PACK ? fb : lb;
-    const uint64_t src0 = PACK ? lb : fb;
-    const uint64_t A = (dst0 & ~uint64_t(15)) + 16u * k;
-    const uint64_t lo_b = A > dst0 ? A : dst0;
-    const uint64_t hi_b = (A + 16u) < (dst0 + nb) ? (A + 16u) : (dst0 + nb);
-    if (lo_b >= hi_b) continue;
-    const uint64_t delta = src0 - dst0;  // modular; source byte of x is x + delta
-    if (lo_b == A && hi_b == A + 16u) {
-      const uint64_t S = A + delta;
-      const uint32_t s = (uint32_t)(S & 15u);
-      const u32x4* L = reinterpret_cast<const u32x4*>(S - s);
-      u32x4 out = L[0];
-      if (s != 0) out = funnel<E>(out, L[1], s);
-#if DIFFOPT_TREE_NT_STORES
-      __builtin_nontemporal_store(out, reinterpret_cast<u32x4*>(A));
+    kind[u] = 0;
+    if (gidx < ngroups) {
+      // largest t with s_goff[t] <= gidx; s_goff[0] <= gidx holds by construction
+      int lo = 0, hi = W - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_goff[mid] <= gidx) lo = mid;
+        else hi = mid - 1;
+      }
+      const uint64_t k = (uint64_t)(gidx - s_goff[lo]);
+      const uint64_t fb = (uint64_t)s_fbase[lo];
+      const uint64_t lb = s_leaf[lo];
+      const uint64_t nb = (uint64_t)s_bytes[lo];
+      const uint64_t dst0 = PACK ? fb : lb;
+      const uint64_t src0 = PACK ? lb : fb;
+      const uint64_t A = (dst0 & ~uint64_t(15)) + 16u * k;
+      lo_b[u] = A > dst0 ? A : dst0;
+      hi_b[u] = (A + 16u) < (dst0 + nb) ? (A + 16u) : (dst0 + nb);
+      delta[u] = src0 - dst0;  // modular; the source byte of x is x + delta
+      dst[u] = A;
+      if (lo_b[u] < hi_b[u]) {
+        if (lo_b[u] == A && hi_b[u] == A + 16u) {
+          kind[u] = 1;
+          const uint64_t S = A + delta[u];
+          shift[u] = (uint32_t)(S & 15u);
+          const u32x4* L = reinterpret_cast<const u32x4*>(S - shift[u]);
+#if DIFFOPT_TREE_NT_LOADS
+          w0[u] = __builtin_nontemporal_load(L);
+          if (shift[u] != 0) w1[u] = __builtin_nontemporal_load(L + 1);
 #else
-      *reinterpret_cast<u32x4*>(A) = out;
+          w0[u] = L[0];
+          if (shift[u] != 0) w1[u] = L[1];
 #endif
-    } else {
-      for (uint64_t x = lo_b; x < hi_b; x += E) {
-        *reinterpret_cast<T*>(x) = *reinterpret_cast<const T*>(x + delta);
+        } else {
+          kind[u] = 2;
+        }
+      }
+    }
+  }
+  typedef typename ElemT<E>::T T;
+#pragma unroll
+  for (int u = 0; u < kTreeU; ++u) {
+    if (kind[u] == 1) {
+      const u32x4 out = shift[u] != 0 ? funnel<E>(w0[u], w1[u], shift[u]) : w0[u];
+#if DIFFOPT_TREE_NT_STORES
+      __builtin_nontemporal_store(out, reinterpret_cast<u32x4*>(dst[u]));
+#else
+      *reinterpret_cast<u32x4*>(dst[u]) = out;
+#endif
+    } else if (kind[u] == 2) {
+      for (uint64_t x = lo_b[u]; x < hi_b[u]; x += E) {
+        *reinterpret_cast<T*>(x) = *reinterpret_cast<const T*>(x + delta[u]);
       }
     }
   }
@@ -197,6 +228,7 @@ struct diffopt_segtable {
   int64_t ntiles = 0;
   int32_t elem_bytes = 4;
   int device = 0;
+  int dense_orig = 1;               // no empty leaves: table index == leaf index
   SegEntry* d_seg = nullptr;       // [nact + 1]
   int64_t* d_tile_first = nullptr;  // [ntiles + 1]
 };
@@ -255,7 +287,8 @@ extern "C" int diffopt_segtable_create(int64_t nseg, const int64_t* numel, const
   t->ngroups = goff;
   t->elem_bytes = elem_bytes;
   t->ntiles = (goff + kTileGroups - 1) / kTileGroups;
-  hipGetDevice(&t->device);
+  t->dense_orig = (nact == nseg) ? 1 : 0;
+  if (hipGetDevice(&t->device) != hipSuccess) t->device = -1;
 
   std::vector<int64_t> tf;
   if (t->ntiles > 0) {
@@ -304,24 +337,27 @@ int tree_copy(const char* who, const diffopt_segtable* t, const uint64_t* leaf_p
   if (!leaf_ptrs || !flat) return fail(DIFFOPT_EINVAL, "%s: null leaf_ptrs or flat", who);
   if (flat % (uint64_t)t->elem_bytes != 0)
     return fail(DIFFOPT_EINVAL, "%s: flat is not aligned to elem_bytes", who);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != t->device)
+    return fail(DIFFOPT_EINVAL, "%s: the table lives on device %d, the current device is %d", who, t->device, dev);
   hipStream_t st = as_stream(stream);
   dim3 grid((unsigned)t->ntiles), block(kTB);
   switch (t->elem_bytes) {
     case 1:
       hipLaunchKernelGGL((tree_copy_kernel<1, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                         leaf_ptrs, flat);
+                         leaf_ptrs, flat, t->dense_orig);
       break;
     case 2:
       hipLaunchKernelGGL((tree_copy_kernel<2, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                         leaf_ptrs, flat);
+                         leaf_ptrs, flat, t->dense_orig);
       break;
     case 4:
       hipLaunchKernelGGL((tree_copy_kernel<4, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                         leaf_ptrs, flat);
+                         leaf_ptrs, flat, t->dense_orig);
       break;
     default:
       hipLaunchKernelGGL((tree_copy_kernel<8, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                         leaf_ptrs, flat);
+                         leaf_ptrs, flat, t->dense_orig);
       break;
   }
   return launch_status(who);
