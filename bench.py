@@ -48,7 +48,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="many_small",
-                    choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10"])
+                    choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
+                             "many_small_treemap"])
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time replays (no per-phase split)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -57,8 +58,12 @@ def parse():
 
 
 KERNEL_SOURCES = {  # the sources each kernel family is built from
-    "adam_fwd": ("adam.hip", "common.hpp"), "adam_bwd": ("adam.hip", "common.hpp"),
-    "tree_flatten": ("tree.hip", "common.hpp"), "tree_unflatten": ("tree.hip", "common.hpp"),
+    "adam_fwd": ("adam.hip", "adam_math.hpp", "common.hpp"),
+    "adam_bwd": ("adam.hip", "adam_math.hpp", "common.hpp"),
+    "tree_flatten": ("tree.hip", "segtable.hpp", "common.hpp"),
+    "tree_unflatten": ("tree.hip", "segtable.hpp", "common.hpp"),
+    "adam_fwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
+    "adam_bwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
 }
 
 
@@ -158,6 +163,59 @@ def phases_tree(S):
         ("adam_bwd", "adam_bwd", K, (B_BWD_FIRST + (K - 1) * B_BWD) * n),
         ("unflatten", "tree_unflatten", K + 1, (K + 1) * B_COPY * n),
     ]
+
+
+def setup_treemap(torch, P, w):
+    """Leaf-direct form of the same pass: every operand is a tree of separately
+    allocated leaves; no flatten or unflatten."""
+    from workloads import HYPER, torch_normal
+    K, n, numel = w.K, w.n, w.numels
+    dev = "cuda"
+
+    def ptrs(leaves):
+        return torch.tensor([x.data_ptr() for x in leaves], dtype=torch.int64).to(dev)
+
+    table = P.segtable_create(numel)
+    trees = []
+
+    def tree(flat=None, zero=False):
+        leaves = [(torch.zeros if zero else torch.empty)(k, dtype=torch.float32, device=dev) for k in numel]
+        if flat is not None:
+            P.tree_unflatten(table, flat, ptrs(leaves))
+        trees.append(leaves)
+        return ptrs(leaves)
+
+    S = dict(K=K, n=n, table=table, hyper=dict(HYPER, eps_root=w.eps_root), count0=w.count0)
+    S["p0"] = tree(torch_normal(n, 0.05, 101, dev))
+    S["g"] = [tree(torch_normal(n, w.grad_std, 110 + k, dev)) for k in range(K)]
+    S["cot"] = tree(torch_normal(n, 1.0, 120, dev))
+    S["mu"] = [tree(zero=True)] + [tree() for _ in range(K)]
+    S["nu"] = [tree(zero=True)] + [tree() for _ in range(K)]
+    S["pK"] = tree()
+    S["dg"] = [tree() for _ in range(K)]
+    S["dm0"], S["dv0"] = tree(), tree()
+    S["keep"] = trees
+    torch.cuda.synchronize()
+    return S
+
+
+def step_treemap(P, S, ev=None):
+    h = S["hyper"]
+    args = (S["count0"], h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+    if ev:
+        ev[0].record()
+    P.adam_unrolled_fwd_tree(S["table"], S["p0"], S["g"], S["mu"], S["nu"], S["pK"], *args)
+    if ev:
+        ev[1].record()
+    P.adam_unrolled_bwd_tree(S["table"], S["cot"], S["g"], S["mu"], S["nu"], S["dg"], S["dm0"], S["dv0"], *args)
+    if ev:
+        ev[2].record()
+
+
+def phases_treemap(S):
+    K, n = S["K"], S["n"]
+    return [("adam_fwd_tree", "adam_fwd_tree", K, K * B_FWD * n),
+            ("adam_bwd_tree", "adam_bwd_tree", K, (B_BWD_FIRST + (K - 1) * B_BWD) * n)]
 
 
 def setup_flat_1b(torch, P, w):
@@ -291,9 +349,11 @@ def main():
     if not torch.cuda.is_available():
         sys.stderr.write("bench.py: no GPU visible\n")
         sys.exit(1)
-    w = WORKLOADS[a.workload]()
+    w = WORKLOADS["many_small" if a.workload == "many_small_treemap" else a.workload]()
     if a.workload == "flat_1b":
         S, step, phases = setup_flat_1b(torch, P, w), step_flat_1b, phases_flat_1b
+    elif a.workload == "many_small_treemap":
+        S, step, phases = setup_treemap(torch, P, w), step_treemap, phases_treemap
     else:
         S, step, phases = setup_tree(torch, P, w), step_tree, phases_tree
     ph = phases(S)
@@ -365,7 +425,7 @@ def main():
                     "avg_launch_us": round(avg_launch_s * 1e6, 2)}
 
     cpu = None
-    if not a.no_cpu_baseline:
+    if not a.no_cpu_baseline and a.workload != "many_small_treemap":
         cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
         cpu["value"] = float("%.4g" % cpu["value"])
 
@@ -373,9 +433,14 @@ def main():
         "metric": METRIC, "value": float("%.6g" % value), "unit": "params/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": w.description, "n_params": n, "leaves": w.nseg, "K": K,
-                   "step": "one Adam fwd + one Adam bwd (count 100, all cotangents)" if a.workload == "flat_1b"
-                   else "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg",
+        "config": {"workload": w.description if a.workload != "many_small_treemap" else
+                   w.description.replace("pack -> K=%d unrolled Adam fwd+bwd -> unpack" % K,
+                                         "leaf-direct K=%d unrolled Adam fwd+bwd (no pack/unpack)" % K),
+                   "n_params": n, "leaves": w.nseg, "K": K,
+                   "step": {"flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",
+                            "many_small_treemap": "leaf-direct K-step Adam fwd -> K-step Adam bwd (no flatten)"}.get(
+                                a.workload,
+                                "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg"),
                    "launch": "hip graph replay" if a.graph else "eager", "parallelism": "single GPU"},
         "us_per_step": round(ms_step * 1e3, 2),
         "achieved_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),

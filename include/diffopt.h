@@ -197,6 +197,65 @@ int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
                               int64_t count0, double lr, double b1, double b2,
                               double eps, double eps_root, void* stream);
 
+
+/* -------------------------------------------------------------------------
+ * Leaf-direct ("tree map") form of the differentiable Adam step (Appendix D,
+ * Table 2 "Tree Map"; Sec. 2.3 for the step): the same forward and VJP as
+ * diffopt_adam_fwd / diffopt_adam_bwd applied to every leaf of parameter
+ * trees, reading and writing the leaves themselves, so no flatten or
+ * unflatten is needed.  The result equals flatten -> flat step -> unflatten
+ * element for element.
+ *   table       a segment table with elem_bytes == 4 describing the leaf
+ *               sizes (its flat offsets are not used); the current device
+ *               must be the table's
+ *   every other pointer argument is a DEVICE array [nseg] of uint64 leaf
+ *               addresses of one operand tree, in table order (entries of
+ *               empty leaves are ignored); leaves are fp32, 4-byte aligned;
+ *               leaves 16-byte aligned in every operand take 128-bit
+ *               accesses, others an element path with the same result
+ * Aliasing as in the flat calls: an output leaf may be its own input leaf
+ * (params_out[j] == params[j], dmu_in[j] == dmu[j], ...), never another leaf.
+ * dmu and dnu are both NULL (zero cotangents) or both given.               */
+int diffopt_adam_fwd_tree(const diffopt_segtable* table, const uint64_t* params,
+                          const uint64_t* grad, const uint64_t* mu,
+                          const uint64_t* nu, int64_t count, double lr,
+                          double b1, double b2, double eps, double eps_root,
+                          const uint64_t* params_out, const uint64_t* mu_out,
+                          const uint64_t* nu_out, void* stream);
+
+int diffopt_adam_bwd_tree(const diffopt_segtable* table, const uint64_t* dupdate,
+                          const uint64_t* dmu, const uint64_t* dnu,
+                          const uint64_t* grad, const uint64_t* mu,
+                          const uint64_t* nu, int64_t count, double lr,
+                          double b1, double b2, double eps, double eps_root,
+                          const uint64_t* dgrad, const uint64_t* dmu_in,
+                          const uint64_t* dnu_in, void* stream);
+
+/* K-step unrolled driver in leaf-direct form: the recurrences of
+ * diffopt_adam_unrolled_fwd / _bwd with every flat buffer replaced by a tree
+ * (a device array of leaf addresses).  grads, mu_traj, nu_traj and dgrads are
+ * HOST arrays ([K], [K+1], [K+1], [K]) of such device arrays; pK is also the
+ * running params tree, dmu0 / dnu0 the running cotangent trees.              */
+int diffopt_adam_unrolled_fwd_tree(const diffopt_segtable* table, int64_t K,
+                                   const uint64_t* p0,
+                                   const uint64_t* const* grads,
+                                   const uint64_t* const* mu_traj,
+                                   const uint64_t* const* nu_traj,
+                                   const uint64_t* pK, int64_t count0, double lr,
+                                   double b1, double b2, double eps,
+                                   double eps_root, void* stream);
+
+int diffopt_adam_unrolled_bwd_tree(const diffopt_segtable* table, int64_t K,
+                                   const uint64_t* dpK,
+                                   const uint64_t* const* grads,
+                                   const uint64_t* const* mu_traj,
+                                   const uint64_t* const* nu_traj,
+                                   const uint64_t* const* dgrads,
+                                   const uint64_t* dmu0, const uint64_t* dnu0,
+                                   int64_t count0, double lr, double b1,
+                                   double b2, double eps, double eps_root,
+                                   void* stream);
+
 #ifdef __cplusplus
 }
 #endif

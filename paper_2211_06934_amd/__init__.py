@@ -1,15 +1,17 @@
 """MI355X-native differentiable-Adam hot path (TorchOpt, arXiv 2211.06934).
 
 The product is the HIP library ``libdiffopt.so`` behind ``include/diffopt.h``:
-fused Adam forward, its fused VJP, a K-step unrolled driver, and tree
-flatten/unflatten through a segment table.  ``diffopt`` is its thin Python
+fused Adam forward, its fused VJP, a K-step unrolled driver, tree
+flatten/unflatten through a segment table, and the leaf-direct ("tree map")
+form of the step that works on the leaves without flattening.  ``diffopt`` is its thin Python
 binding (same entry points), ``tree`` the host-side container walk and
 ``autograd`` a torch.autograd.Function over the fused step.  Importing the
 package loads the library and raises ImportError if it has not been built.
 """
 from . import diffopt
-from .diffopt import (DiffoptError, SegTable, adam_bwd, adam_fwd, adam_unrolled_bwd,
-                      adam_unrolled_fwd, last_error, segtable_create, segtable_destroy,
+from .diffopt import (DiffoptError, SegTable, adam_bwd, adam_bwd_tree, adam_fwd, adam_fwd_tree,
+                      adam_unrolled_bwd, adam_unrolled_bwd_tree, adam_unrolled_fwd,
+                      adam_unrolled_fwd_tree, last_error, segtable_create, segtable_destroy,
                       segtable_nseg, segtable_total, tree_flatten, tree_unflatten)
 from . import tree
 from . import autograd
@@ -17,7 +19,8 @@ from .autograd import AdamFn, AdamHyper, AdamState, FlatAdam
 
 __all__ = [
     "diffopt", "tree", "autograd", "DiffoptError", "SegTable", "adam_bwd", "adam_fwd",
-    "adam_unrolled_bwd", "adam_unrolled_fwd", "last_error", "segtable_create", "segtable_destroy",
+    "adam_unrolled_bwd", "adam_unrolled_fwd", "adam_fwd_tree", "adam_bwd_tree",
+    "adam_unrolled_fwd_tree", "adam_unrolled_bwd_tree", "last_error", "segtable_create", "segtable_destroy",
     "segtable_nseg", "segtable_total", "tree_flatten", "tree_unflatten", "AdamFn", "AdamHyper",
     "AdamState", "FlatAdam",
 ]

@@ -1,0 +1,55 @@
+// Device segment table shared by tree flatten / unflatten (tree.hip) and the
+// leaf-direct Adam kernels (treemap.hip): the group index space, the tile plan
+// and the window bound.
+#pragma once
+
+#include "common.hpp"
+
+// Launch shape, chosen by measurement on MI355X (20,000 leaves, n ~ 1.2e8):
+// 256 threads x 2 groups per tile with streaming stores.  One group per lane
+// (any workgroup size) spends too long per staged window; 4 groups per lane,
+// and renumbering tiles so that each XCD walks a contiguous run, were slower.
+#ifndef DIFFOPT_TREE_U
+#define DIFFOPT_TREE_U 2  // groups (16-byte vectors) per lane per tile
+#endif
+#ifndef DIFFOPT_TREE_BLOCK
+#define DIFFOPT_TREE_BLOCK 256  // threads per workgroup of the copy kernel
+#endif
+#ifndef DIFFOPT_TREE_NT_LOADS
+#define DIFFOPT_TREE_NT_LOADS 0  // streaming loads of source vectors
+#endif
+#ifndef DIFFOPT_TREE_NT_STORES
+#define DIFFOPT_TREE_NT_STORES 1  // streaming stores of full destination vectors
+#endif
+
+namespace diffopt {
+
+constexpr int kTreeU = DIFFOPT_TREE_U;
+constexpr int kTB = DIFFOPT_TREE_BLOCK;
+constexpr int64_t kTileGroups = (int64_t)kTB * kTreeU;
+constexpr int kWindowMax = (int)(kTileGroups / 2 + 2);
+
+// One nonempty leaf, in table order.  The entry after the last nonempty leaf
+// is a sentinel whose goff is the total group count.
+struct SegEntry {
+  int64_t goff;   // first group index
+  int64_t off;    // flat element offset
+  int64_t numel;  // elements
+  int64_t orig;   // index into the caller's leaf-address array
+};
+
+}  // namespace diffopt
+
+struct diffopt_segtable {
+  int64_t nseg = 0;
+  int64_t total = 0;
+  int64_t nact = 0;
+  int64_t ngroups = 0;
+  int64_t ntiles = 0;
+  int32_t elem_bytes = 4;
+  int device = 0;
+  int dense_orig = 1;               // no empty leaves: table index == leaf index
+  diffopt::SegEntry* d_seg = nullptr;       // [nact + 1]
+  int64_t* d_tile_first = nullptr;  // [ntiles + 1]
+};
+

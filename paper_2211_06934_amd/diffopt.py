@@ -49,6 +49,10 @@ def _load_library():
         "diffopt_adam_bwd": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, *hyper, vp, vp, vp, vp, vp]),
         "diffopt_adam_unrolled_fwd": (ctypes.c_int, [i64, i64, vp, pp, pp, pp, vp, *hyper, vp]),
         "diffopt_adam_unrolled_bwd": (ctypes.c_int, [i64, i64, vp, pp, pp, pp, pp, vp, vp, *hyper, vp]),
+        "diffopt_adam_fwd_tree": (ctypes.c_int, [vp, vp, vp, vp, vp, *hyper, vp, vp, vp, vp]),
+        "diffopt_adam_bwd_tree": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, *hyper, vp, vp, vp, vp]),
+        "diffopt_adam_unrolled_fwd_tree": (ctypes.c_int, [vp, i64, vp, pp, pp, pp, vp, *hyper, vp]),
+        "diffopt_adam_unrolled_bwd_tree": (ctypes.c_int, [vp, i64, vp, pp, pp, pp, pp, vp, vp, *hyper, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -223,3 +227,73 @@ def adam_unrolled_bwd(dpK, grads, mu_traj, nu_traj, dgrads, dmu0, dnu0, count0, 
         _ptr_array(nu_traj[:K], "nu_traj", n), _ptr_array(dgrads, "dgrads", n), _addr(dmu0, "dmu0", n=n),
         _addr(dnu0, "dnu0", n=n), int(count0), float(lr), float(b1), float(b2), float(eps), float(eps_root),
         _stream(stream)))
+
+
+# ---- leaf-direct ("tree map") form: every operand is a device int64 tensor of
+# leaf addresses in table order (see tree.leaf_pointer_tensor)
+
+
+def _leaf_array(x, what, nseg):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return _addr(x, what, torch.int64, n=nseg)
+
+
+def _leaf_array_list(items, what, nseg):
+    arr = (ctypes.c_void_p * len(items))()
+    for i, t in enumerate(items):
+        arr[i] = _leaf_array(t, "%s[%d]" % (what, i), nseg)
+    return arr
+
+
+def adam_fwd_tree(table: SegTable, params, grad, mu, nu, count, lr, b1, b2, eps, eps_root,
+                  params_out, mu_out, nu_out, stream=None) -> None:
+    """diffopt_adam_fwd_tree."""
+    k = len(table.numel)
+    _check(_lib.diffopt_adam_fwd_tree(
+        table.handle, *[_leaf_array(x, w, k) for x, w in ((params, "params"), (grad, "grad"), (mu, "mu"),
+                                                           (nu, "nu"))],
+        int(count), float(lr), float(b1), float(b2), float(eps), float(eps_root),
+        *[_leaf_array(x, w, k) for x, w in ((params_out, "params_out"), (mu_out, "mu_out"), (nu_out, "nu_out"))],
+        _stream(stream)))
+
+
+def adam_bwd_tree(table: SegTable, dupdate, dmu, dnu, grad, mu, nu, count, lr, b1, b2, eps, eps_root,
+                  dgrad, dmu_in, dnu_in, stream=None) -> None:
+    """diffopt_adam_bwd_tree; dmu/dnu may be None."""
+    k = len(table.numel)
+    _check(_lib.diffopt_adam_bwd_tree(
+        table.handle, *[_leaf_array(x, w, k) for x, w in ((dupdate, "dupdate"), (dmu, "dmu"), (dnu, "dnu"),
+                                                           (grad, "grad"), (mu, "mu"), (nu, "nu"))],
+        int(count), float(lr), float(b1), float(b2), float(eps), float(eps_root),
+        *[_leaf_array(x, w, k) for x, w in ((dgrad, "dgrad"), (dmu_in, "dmu_in"), (dnu_in, "dnu_in"))],
+        _stream(stream)))
+
+
+def adam_unrolled_fwd_tree(table: SegTable, p0, grads, mu_traj, nu_traj, pK, count0, lr, b1, b2, eps, eps_root,
+                           stream=None) -> None:
+    """diffopt_adam_unrolled_fwd_tree; grads has K entries, mu_traj/nu_traj K+1."""
+    K = len(grads)
+    k = len(table.numel)
+    if len(mu_traj) != K + 1 or len(nu_traj) != K + 1:
+        raise ValueError("mu_traj and nu_traj need K+1 entries")
+    _check(_lib.diffopt_adam_unrolled_fwd_tree(
+        table.handle, K, _leaf_array(p0, "p0", k), _leaf_array_list(grads, "grads", k),
+        _leaf_array_list(mu_traj, "mu_traj", k), _leaf_array_list(nu_traj, "nu_traj", k), _leaf_array(pK, "pK", k),
+        int(count0), float(lr), float(b1), float(b2), float(eps), float(eps_root), _stream(stream)))
+
+
+def adam_unrolled_bwd_tree(table: SegTable, dpK, grads, mu_traj, nu_traj, dgrads, dmu0, dnu0, count0, lr, b1, b2,
+                           eps, eps_root, stream=None) -> None:
+    """diffopt_adam_unrolled_bwd_tree; mu_traj/nu_traj may hold K or K+1 entries."""
+    K = len(grads)
+    k = len(table.numel)
+    if len(dgrads) != K or len(mu_traj) < K or len(nu_traj) < K:
+        raise ValueError("dgrads needs K entries, mu_traj/nu_traj at least K")
+    _check(_lib.diffopt_adam_unrolled_bwd_tree(
+        table.handle, K, _leaf_array(dpK, "dpK", k), _leaf_array_list(grads, "grads", k),
+        _leaf_array_list(mu_traj[:K], "mu_traj", k), _leaf_array_list(nu_traj[:K], "nu_traj", k),
+        _leaf_array_list(dgrads, "dgrads", k), _leaf_array(dmu0, "dmu0", k), _leaf_array(dnu0, "dnu0", k),
+        int(count0), float(lr), float(b1), float(b2), float(eps), float(eps_root), _stream(stream)))
