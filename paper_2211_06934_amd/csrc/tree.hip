@@ -4,11 +4,13 @@
 // Work decomposition.  Every copy writes whole, naturally aligned 16-byte
 // vectors of its DESTINATION (the flat buffer for flatten, the leaves for
 // unflatten).  Nonempty leaf j owns G_j = ceil(bytes_j / 16) + 1 consecutive
-// "groups" of a global group index space; group k of leaf j is the aligned
-// 16-byte destination vector number k counted from the vector that holds the
-// leaf's first destination byte.  The +1 covers any alignment phase, so the
-// G_j groups always cover the leaf; a group may be partial (head, tail) or
-// empty.  Each lane owns one group per step: full groups take one aligned
+// "groups" of a global group index space, rounded up to a multiple of 8; group
+// k of leaf j is the aligned 16-byte destination vector number k counted from
+// the vector that holds the leaf's first destination byte.  The +1 covers any
+// alignment phase, so the G_j groups always cover the leaf; a group may be
+// partial (head, tail) or empty.  The rounding starts every leaf on a 128-byte
+// boundary of the group space, so for line-aligned destinations (leaves from an
+// allocator) tile boundaries never split a cache line between two tiles.  Each lane owns one group per step: full groups take one aligned
 // 128-bit store, fed by one or two aligned 128-bit loads of the source and a
 // funnel shift when source and destination phases differ (dense offsets put
 // ~3/4 of leaves out of phase with their flat range); partial groups copy
@@ -20,7 +22,7 @@
 // touches are the window tile_first[b] .. tile_first[b+1].  The block stages
 // that window (group offsets, flat offsets, byte sizes, leaf addresses) in LDS
 // once, then every lane binary-searches the LDS window for its group.  Since
-// every nonempty leaf owns >= 2 groups, a window never exceeds TG/2 + 2
+// every nonempty leaf owns >= 8 groups, a window never exceeds TG/8 + 1
 // leaves, which bounds the LDS footprint.
 //
 // Page safety of the two source loads: a full group's 16 source bytes are all
@@ -220,7 +222,8 @@ extern "C" int diffopt_segtable_create(int64_t nseg, const int64_t* numel, const
     run = off + k;
     if (k == 0) continue;
     total = std::max(total, off + k);
-    const int64_t groups = (k * elem_bytes + 15) / 16 + 1;
+    const int64_t need = (k * elem_bytes + 15) / 16 + 1;  // +1 absorbs any destination phase
+    const int64_t groups = (need + kLeafGroupAlign - 1) / kLeafGroupAlign * kLeafGroupAlign;
     host.push_back(SegEntry{goff, off, k, j});
     ranges.emplace_back(off, off + k);
     goff += groups;

@@ -6,7 +6,9 @@
 //
 // Work decomposition: the segment table of tree.hip.  Group k of nonempty
 // leaf j covers the leaf's elements [4k, 4k + 4); the table gives each leaf
-// ceil(numel / 4) + 1 groups, so the last one is always empty here.  A
+// ceil(numel / 4) + 1 groups rounded up to a multiple of 8, so the last ones
+// are empty here.  Leaves start on 8-group boundaries, so for 128-byte aligned
+// leaves no cache line is shared by two tiles (which run on different XCDs).  A
 // workgroup stages its window of the table in LDS together with the leaf
 // addresses of every operand tree, each lane binary-searches the window for
 // its groups, issues every operand load of all of its groups, then computes
