@@ -15,12 +15,12 @@ from .diffopt import (DiffoptError, SegTable, adam_bwd, adam_bwd_tree, adam_fwd,
                       segtable_nseg, segtable_total, tree_flatten, tree_unflatten)
 from . import tree
 from . import autograd
-from .autograd import AdamFn, AdamHyper, AdamState, FlatAdam
+from .autograd import AdamFn, AdamHyper, AdamState, AdamTreeFn, FlatAdam, MetaAdam
 
 __all__ = [
     "diffopt", "tree", "autograd", "DiffoptError", "SegTable", "adam_bwd", "adam_fwd",
     "adam_unrolled_bwd", "adam_unrolled_fwd", "adam_fwd_tree", "adam_bwd_tree",
     "adam_unrolled_fwd_tree", "adam_unrolled_bwd_tree", "last_error", "segtable_create", "segtable_destroy",
     "segtable_nseg", "segtable_total", "tree_flatten", "tree_unflatten", "AdamFn", "AdamHyper",
-    "AdamState", "FlatAdam",
+    "AdamState", "FlatAdam", "AdamTreeFn", "MetaAdam",
 ]
