@@ -56,7 +56,16 @@ def _load():
                                     ctypes.POINTER(vp), vp]
         lib.oracle_unpack.argtypes = [i64, ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
                                       vp, ctypes.POINTER(vp)]
-        for f in ("oracle_adam_fwd", "oracle_adam_bwd", "oracle_adam_fwd_mag",
+        lib.oracle_sgd_fwd.argtypes = [i64, d, d, d, f64, f64, i64, d, d]
+        lib.oracle_sgd_bwd.argtypes = [i64, d, d, f64, f64, i64, d, d]
+        rms = [f64, f64, f64, f64, f64]  # lr, alpha, eps, eps_root, mu
+        lib.oracle_rmsprop_fwd.argtypes = [i64, d, d, d, d, *rms, d, d, d]
+        lib.oracle_rmsprop_bwd.argtypes = [i64, d, d, d, d, d, *rms, d, d, d]
+        lib.oracle_rmsprop_fwd_mag.argtypes = [i64, d, d, d, d, *rms, d, d, d]
+        lib.oracle_rmsprop_bwd_mag.argtypes = [i64, d, d, d, d, d, *rms, d, d, d]
+        for f in ("oracle_sgd_fwd", "oracle_sgd_bwd", "oracle_rmsprop_fwd", "oracle_rmsprop_bwd",
+                  "oracle_rmsprop_fwd_mag", "oracle_rmsprop_bwd_mag",
+                  "oracle_adam_fwd", "oracle_adam_bwd", "oracle_adam_fwd_mag",
                   "oracle_adam_bwd_mag", "oracle_unrolled_fwd", "oracle_unrolled_bwd",
                   "oracle_pack", "oracle_unpack"):
             getattr(lib, f).restype = None
@@ -203,3 +212,75 @@ def unpack(flat, shapes, offsets=None):
     ptrs = (ctypes.c_void_p * max(len(leaves), 1))(*[x.ctypes.data for x in leaves])
     _load().oracle_unpack(len(leaves), pn, po, flat.dtype.itemsize, flat.ctypes.data, ptrs)
     return leaves
+
+
+def _opt(x, n):
+    return None if x is None else _f64(x, n)
+
+
+def sgd_fwd(p, g, t, lr, momentum=0.0, nesterov=False):
+    """SGD with momentum; t may be None (zero trace).  Returns (p', t')."""
+    p = _f64(p)
+    n = p.size
+    g, t = _f64(g, n), _opt(t, n)
+    po, to = np.empty(n), np.empty(n)
+    _load().oracle_sgd_fwd(n, _ptr(p), _ptr(g), _ptr(t), float(lr), float(momentum), int(bool(nesterov)),
+                           _ptr(po), _ptr(to))
+    return po, to
+
+
+def sgd_bwd(dP, dT, lr, momentum=0.0, nesterov=False):
+    """VJP of sgd_fwd; dT may be None.  Returns (dp, dg, dt)."""
+    dP = _f64(dP)
+    n = dP.size
+    dT = _opt(dT, n)
+    dg, dt = np.empty(n), np.empty(n)
+    _load().oracle_sgd_bwd(n, _ptr(dP), _ptr(dT), float(lr), float(momentum), int(bool(nesterov)), _ptr(dg),
+                           _ptr(dt))
+    return dP.copy(), dg, dt
+
+
+def rmsprop_fwd(p, g, v, b, lr, alpha=0.99, eps=1e-8, eps_root=0.0, momentum=0.0):
+    """RMSProp; b may be None.  Returns (p', v', b') (b' is zeros when momentum == 0)."""
+    p = _f64(p)
+    n = p.size
+    g, v, b = _f64(g, n), _f64(v, n), _opt(b, n)
+    po, vo, bo = np.empty(n), np.empty(n), np.zeros(n)
+    _load().oracle_rmsprop_fwd(n, _ptr(p), _ptr(g), _ptr(v), _ptr(b), float(lr), float(alpha), float(eps),
+                               float(eps_root), float(momentum), _ptr(po), _ptr(vo), _ptr(bo))
+    return po, vo, bo
+
+
+def rmsprop_bwd(dP, dV, dB, g, v, lr, alpha=0.99, eps=1e-8, eps_root=0.0, momentum=0.0):
+    """VJP of rmsprop_fwd; dV, dB may be None.  Returns (dp, dg, dv, db)."""
+    dP = _f64(dP)
+    n = dP.size
+    dV, dB = _opt(dV, n), _opt(dB, n)
+    g, v = _f64(g, n), _f64(v, n)
+    dg, dv, db = np.empty(n), np.empty(n), np.zeros(n)
+    _load().oracle_rmsprop_bwd(n, _ptr(dP), _ptr(dV), _ptr(dB), _ptr(g), _ptr(v), float(lr), float(alpha),
+                               float(eps), float(eps_root), float(momentum), _ptr(dg), _ptr(dv), _ptr(db))
+    return dP.copy(), dg, dv, db
+
+
+def rmsprop_fwd_mag(p, g, v, b, lr, alpha=0.99, eps=1e-8, eps_root=0.0, momentum=0.0):
+    """Tolerance scales (mag_p, mag_v, mag_b) of rmsprop_fwd."""
+    p = _f64(p)
+    n = p.size
+    g, v, b = _f64(g, n), _f64(v, n), _opt(b, n)
+    out = [np.empty(n) for _ in range(3)]
+    _load().oracle_rmsprop_fwd_mag(n, _ptr(p), _ptr(g), _ptr(v), _ptr(b), float(lr), float(alpha), float(eps),
+                                   float(eps_root), float(momentum), *map(_ptr, out))
+    return tuple(out)
+
+
+def rmsprop_bwd_mag(dP, dV, dB, g, v, lr, alpha=0.99, eps=1e-8, eps_root=0.0, momentum=0.0):
+    """Tolerance scales (mag_dg, mag_dv, mag_db) of rmsprop_bwd."""
+    dP = _f64(dP)
+    n = dP.size
+    dV, dB = _opt(dV, n), _opt(dB, n)
+    g, v = _f64(g, n), _f64(v, n)
+    out = [np.empty(n) for _ in range(3)]
+    _load().oracle_rmsprop_bwd_mag(n, _ptr(dP), _ptr(dV), _ptr(dB), _ptr(g), _ptr(v), float(lr), float(alpha),
+                                   float(eps), float(eps_root), float(momentum), *map(_ptr, out))
+    return tuple(out)

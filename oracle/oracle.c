@@ -292,3 +292,127 @@ void oracle_unpack(int64_t nseg, const int64_t* numel, const int64_t* offsets,
     run += numel[j];
   }
 }
+
+/* ---------------------------------------------------------------------------
+ * The paper's other fused differentiable optimizers (Sec. 1, contribution
+ * (2)(i): SGD, RMSProp, Adam).  It prints no formula for them either; these
+ * are the textbook forms, as torch.optim implements them.
+ *
+ * SGD with momentum mu >= 0 (trace t, zero initially; mu = 0 is plain SGD):
+ *   t' = mu t + g
+ *   u  = -lr t'                (nesterov: u = -lr (g + mu t'))
+ *   p' = p + u
+ * t_out may be NULL when mu == 0 (no state).
+ */
+void oracle_sgd_fwd(int64_t n, const double* p, const double* g, const double* t, double lr, double mu,
+                    int64_t nesterov, double* p_out, double* t_out) {
+  for (int64_t i = 0; i < n; ++i) {
+    double t1 = (t ? mu * t[i] : 0.0) + g[i];
+    double u = nesterov ? -lr * (g[i] + mu * t1) : -lr * t1;
+    if (t_out) t_out[i] = t1;
+    p_out[i] = p[i] + u;
+  }
+}
+
+/* VJP of oracle_sgd_fwd, chain rule.  Cotangents dP on p', dT on t' (NULL =
+ * zero).  dL/dt' = dT - lr dP (nesterov: dT - lr mu dP);
+ *   dg = dL/dt' (+ nesterov: - lr dP),  dt = mu dL/dt',  dp = dP.
+ * The map is linear, so the VJP does not depend on p, g or t. */
+void oracle_sgd_bwd(int64_t n, const double* dP, const double* dT, double lr, double mu, int64_t nesterov,
+                    double* dg_out, double* dt_out) {
+  for (int64_t i = 0; i < n; ++i) {
+    double dTi = dT ? dT[i] : 0.0;
+    double Tt = dTi - (nesterov ? lr * mu : lr) * dP[i];
+    dg_out[i] = Tt - (nesterov ? lr * dP[i] : 0.0);
+    if (dt_out) dt_out[i] = mu * Tt;
+  }
+}
+
+/*
+ * RMSProp with decay alpha in [0, 1), eps outside and eps_root inside the
+ * root, optional momentum mu >= 0 (buffer b, zero initially):
+ *   v' = alpha v + (1-alpha) g^2
+ *   s  = sqrt(v' + eps_root),  d = s + eps
+ *   mu == 0:  u = -lr g / d
+ *   mu >  0:  b' = mu b + g / d,  u = -lr b'
+ *   p' = p + u
+ * b, b_out are unused (may be NULL) when mu == 0.
+ */
+void oracle_rmsprop_fwd(int64_t n, const double* p, const double* g, const double* v, const double* b, double lr,
+                        double alpha, double eps, double eps_root, double mu, double* p_out, double* v_out,
+                        double* b_out) {
+  for (int64_t i = 0; i < n; ++i) {
+    double v1 = alpha * v[i] + (1.0 - alpha) * g[i] * g[i];
+    double s = sqrt(v1 + eps_root);
+    double d = s + eps;
+    double q = g[i] / d;
+    double u;
+    if (mu > 0.0) {
+      double b1 = mu * (b ? b[i] : 0.0) + q;
+      if (b_out) b_out[i] = b1;
+      u = -lr * b1;
+    } else {
+      u = -lr * q;
+    }
+    v_out[i] = v1;
+    p_out[i] = p[i] + u;
+  }
+}
+
+/* VJP of oracle_rmsprop_fwd, plain chain rule.  Cotangents dP on p', dV on v',
+ * dB on b' (dV, dB NULL = zero; dB unused when mu == 0).
+ *   Bt = dB - lr dP            (mu > 0: cotangent of b');  mu == 0: Bt = -lr dP
+ *   dL/d(g/d) = Bt
+ *   Vt = dV - Bt g / (2 s d^2)   (the Bt term := 0 when s == 0, reading R3)
+ *   dg = Bt / d + 2 (1-alpha) g Vt,  dv = alpha Vt,  db = mu Bt,  dp = dP
+ * At s == 0 (eps_root = 0, v = 0, g = 0) this gives dg's Bt term Bt / eps,
+ * the symmetric derivative of g / d at g = 0. */
+void oracle_rmsprop_bwd(int64_t n, const double* dP, const double* dV, const double* dB, const double* g,
+                        const double* v, double lr, double alpha, double eps, double eps_root, double mu,
+                        double* dg_out, double* dv_out, double* db_out) {
+  for (int64_t i = 0; i < n; ++i) {
+    double v1 = alpha * v[i] + (1.0 - alpha) * g[i] * g[i];
+    double s = sqrt(v1 + eps_root);
+    double d = s + eps;
+    double Bt = (mu > 0.0 ? (dB ? dB[i] : 0.0) : 0.0) - lr * dP[i];
+    double Vt = dV ? dV[i] : 0.0;
+    if (s > 0.0) Vt -= Bt * g[i] / (2.0 * s * d * d);
+    dg_out[i] = Bt / d + 2.0 * (1.0 - alpha) * g[i] * Vt;
+    dv_out[i] = alpha * Vt;
+    if (db_out) db_out[i] = mu * Bt;
+  }
+}
+
+/* Tolerance scales for RMSProp (sums of |terms|; for dg taken from the
+ * algebraically reduced form dg = 2(1-alpha) g dV + Bt (alpha v + eps_root +
+ * s eps) / (s d^2), in which the g^2 terms of the chain rule cancel). */
+void oracle_rmsprop_fwd_mag(int64_t n, const double* p, const double* g, const double* v, const double* b,
+                            double lr, double alpha, double eps, double eps_root, double mu, double* mag_p,
+                            double* mag_v, double* mag_b) {
+  for (int64_t i = 0; i < n; ++i) {
+    double v1 = alpha * fabs(v[i]) + (1.0 - alpha) * g[i] * g[i];
+    double s = sqrt(alpha * v[i] + (1.0 - alpha) * g[i] * g[i] + eps_root);
+    double d = s + eps;
+    double aq = fabs(g[i]) / d;
+    double ab = mu > 0.0 ? mu * fabs(b ? b[i] : 0.0) + aq : aq;
+    mag_v[i] = v1;
+    if (mag_b) mag_b[i] = ab;
+    mag_p[i] = fabs(p[i]) + lr * ab;
+  }
+}
+
+void oracle_rmsprop_bwd_mag(int64_t n, const double* dP, const double* dV, const double* dB, const double* g,
+                            const double* v, double lr, double alpha, double eps, double eps_root, double mu,
+                            double* mag_dg, double* mag_dv, double* mag_db) {
+  for (int64_t i = 0; i < n; ++i) {
+    double s = sqrt(alpha * v[i] + (1.0 - alpha) * g[i] * g[i] + eps_root);
+    double d = s + eps;
+    double aBt = (mu > 0.0 ? fabs(dB ? dB[i] : 0.0) : 0.0) + lr * fabs(dP[i]);
+    double adV = dV ? fabs(dV[i]) : 0.0;
+    double t3 = s > 0.0 ? aBt * (alpha * fabs(v[i]) + eps_root + s * eps) / (s * d * d) : aBt / d;
+    double tv = s > 0.0 ? aBt * fabs(g[i]) / (2.0 * s * d * d) : 0.0;
+    mag_dg[i] = 2.0 * (1.0 - alpha) * fabs(g[i]) * adV + t3;
+    mag_dv[i] = alpha * (adV + tv);
+    if (mag_db) mag_db[i] = mu * aBt;
+  }
+}
