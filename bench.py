@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="many_small",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
-                             "many_small_treemap"])
+                             "many_small_treemap", "sgd_flat", "rmsprop_flat"])
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time replays (no per-phase split)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -64,6 +64,9 @@ KERNEL_SOURCES = {  # the sources each kernel family is built from
     "tree_unflatten": ("tree.hip", "segtable.hpp", "common.hpp"),
     "adam_fwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
     "adam_bwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
+    "sgd_fwd": ("optim.hip", "adam_math.hpp", "common.hpp"), "sgd_bwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
+    "rmsprop_fwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
+    "rmsprop_bwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
 }
 
 
@@ -244,6 +247,51 @@ def step_flat_1b(P, S, ev=None):
         ev[2].record()
 
 
+N_OPTIM = 117_000_292  # the many-small tree's parameter count, as one flat buffer
+
+
+def setup_optim(torch, P, which):
+    """One interior step of fused SGD-momentum (Nesterov) or RMSProp with
+    momentum on a flat buffer: every optional state and cotangent present."""
+    from workloads import torch_normal
+    n, dev = N_OPTIM, "cuda"
+    r = lambda seed, std=1.0: torch_normal(n, std, seed, dev)  # noqa: E731
+    e = lambda: torch.empty(n, dtype=torch.float32, device=dev)  # noqa: E731
+    S = dict(K=1, n=n, which=which, p=r(301, 0.05), g=r(302, 0.01), dP=r(305), po=e(), dg=e())
+    if which == "sgd":
+        S.update(t=r(303, 0.01), to=e(), dT=r(306), dt=e(), lr=0.05, mom=0.9)
+    else:
+        S.update(v=r(303, 1e-4).abs_(), b=r(304, 0.1), vo=e(), bo=e(), dV=r(306), dB=r(307), dv=e(), db=e(),
+                 lr=1e-3, mom=0.9)
+    return S
+
+
+def step_optim(P, S, ev=None):
+    if ev:
+        ev[0].record()
+    if S["which"] == "sgd":
+        P.sgd_fwd(S["p"], S["g"], S["t"], S["lr"], S["mom"], True, S["po"], S["to"])
+    else:
+        P.rmsprop_fwd(S["p"], S["g"], S["v"], S["b"], S["lr"], 0.99, 1e-8, 0.0, S["mom"], S["po"], S["vo"], S["bo"])
+    if ev:
+        ev[1].record()
+    if S["which"] == "sgd":
+        P.sgd_bwd(S["dP"], S["dT"], S["lr"], S["mom"], True, S["dg"], S["dt"])
+    else:
+        P.rmsprop_bwd(S["dP"], S["dV"], S["dB"], S["g"], S["v"], S["lr"], 0.99, 1e-8, 0.0, S["mom"], S["dg"],
+                      S["dv"], S["db"])
+    if ev:
+        ev[2].record()
+
+
+def phases_optim(S):
+    n = S["n"]
+    if S["which"] == "sgd":  # fwd: p, g, t -> p', t'; bwd: dP, dT -> dg, dt
+        return [("sgd_fwd", "sgd_fwd", 1, 20 * n), ("sgd_bwd", "sgd_bwd", 1, 16 * n)]
+    # fwd: p, g, v, b -> p', v', b'; bwd: dP, dV, dB, g, v -> dg, dv, db
+    return [("rmsprop_fwd", "rmsprop_fwd", 1, 28 * n), ("rmsprop_bwd", "rmsprop_bwd", 1, 32 * n)]
+
+
 def phases_flat_1b(S):
     n = S["n"]
     return [("adam_fwd", "adam_fwd", 1, B_FWD * n), ("adam_bwd", "adam_bwd", 1, B_BWD * n)]
@@ -349,8 +397,11 @@ def main():
     if not torch.cuda.is_available():
         sys.stderr.write("bench.py: no GPU visible\n")
         sys.exit(1)
-    w = WORKLOADS["many_small" if a.workload == "many_small_treemap" else a.workload]()
-    if a.workload == "flat_1b":
+    w = WORKLOADS["many_small" if a.workload in ("many_small_treemap", "sgd_flat", "rmsprop_flat")
+                  else a.workload]()
+    if a.workload in ("sgd_flat", "rmsprop_flat"):
+        S, step, phases = setup_optim(torch, P, a.workload.split("_")[0]), step_optim, phases_optim
+    elif a.workload == "flat_1b":
         S, step, phases = setup_flat_1b(torch, P, w), step_flat_1b, phases_flat_1b
     elif a.workload == "many_small_treemap":
         S, step, phases = setup_treemap(torch, P, w), step_treemap, phases_treemap
@@ -425,7 +476,7 @@ def main():
                     "avg_launch_us": round(avg_launch_s * 1e6, 2)}
 
     cpu = None
-    if not a.no_cpu_baseline and a.workload != "many_small_treemap":
+    if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat"):
         cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
         cpu["value"] = float("%.4g" % cpu["value"])
 
@@ -433,9 +484,13 @@ def main():
         "metric": METRIC, "value": float("%.6g" % value), "unit": "params/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": w.description if a.workload != "many_small_treemap" else
-                   w.description.replace("pack -> K=%d unrolled Adam fwd+bwd -> unpack" % K,
-                                         "leaf-direct K=%d unrolled Adam fwd+bwd (no pack/unpack)" % K),
+        "config": {"workload": {
+                       "many_small_treemap": w.description.replace(
+                           "pack -> K=%d unrolled Adam fwd+bwd -> unpack" % K,
+                           "leaf-direct K=%d unrolled Adam fwd+bwd (no pack/unpack)" % K),
+                       "sgd_flat": "flat fp32 buffer, n=%d, one Nesterov SGD-momentum fwd + bwd" % n,
+                       "rmsprop_flat": "flat fp32 buffer, n=%d, one RMSProp-momentum fwd + bwd" % n,
+                   }.get(a.workload, w.description),
                    "n_params": n, "leaves": w.nseg, "K": K,
                    "step": {"flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",
                             "many_small_treemap": "leaf-direct K-step Adam fwd -> K-step Adam bwd (no flatten)"}.get(

@@ -256,6 +256,54 @@ int diffopt_adam_unrolled_bwd_tree(const diffopt_segtable* table, int64_t K,
                                    double b2, double eps, double eps_root,
                                    void* stream);
 
+/* -------------------------------------------------------------------------
+ * The paper's other fused differentiable optimizers (Sec. 1, contribution
+ * (2)(i): SGD, RMSProp, Adam; Sec. 2.3).  The paper prints no formula; these
+ * are the textbook forms as torch.optim implements them.  Conventions as for
+ * Adam: fp32 device buffers [n], scalars in fp64, n == 0 is a no-op, outputs
+ * may alias their own inputs, state buffers that are NULL read as zero.
+ *
+ * SGD with momentum mu >= 0 (trace t):
+ *   t' = mu t + g;  u = -lr t'  (nesterov != 0: u = -lr (g + mu t'));  p' = p + u
+ *   mu == 0 is plain SGD: trace and trace_out are ignored (may be NULL).
+ *   mu  > 0: trace may be NULL (zero, the first step); trace_out required.  */
+int diffopt_sgd_fwd(const float* params, const float* grad, const float* trace,
+                    int64_t n, double lr, double momentum, int32_t nesterov,
+                    float* params_out, float* trace_out, void* stream);
+
+/* VJP of diffopt_sgd_fwd.  dparams_out: cotangent of p' (the cotangent of p
+ * is the same array); dtrace_out: cotangent of t' (NULL = zero).  Writes the
+ * cotangent of g and, when mu > 0, of t (dtrace_in, required then).  The map
+ * is linear, so no forward input is needed.                               */
+int diffopt_sgd_bwd(const float* dparams_out, const float* dtrace_out,
+                    int64_t n, double lr, double momentum, int32_t nesterov,
+                    float* dgrad, float* dtrace_in, void* stream);
+
+/* RMSProp with decay alpha in [0, 1), eps >= 0 outside and eps_root >= 0
+ * inside the root, momentum mu >= 0 (buffer b):
+ *   v' = alpha v + (1-alpha) g^2;  d = sqrt(v' + eps_root) + eps
+ *   mu == 0: u = -lr g / d          (mom, mom_out ignored)
+ *   mu  > 0: b' = mu b + g / d, u = -lr b'   (mom may be NULL; mom_out required)
+ *   p' = p + u                                                             */
+int diffopt_rmsprop_fwd(const float* params, const float* grad, const float* nu,
+                        const float* mom, int64_t n, double lr, double alpha,
+                        double eps, double eps_root, double momentum,
+                        float* params_out, float* nu_out, float* mom_out,
+                        void* stream);
+
+/* VJP of diffopt_rmsprop_fwd, in the algebraically reduced form (the g^2
+ * terms of the chain rule cancel).  Cotangents of p', v', b' (dnu_out and
+ * dmom_out may be NULL = zero); grad and nu are the forward's INPUTS.
+ * Writes the cotangents of g, v and, when mu > 0, of b (dmom_in required).
+ * At the 0/0 point (eps_root = 0, v = 0, g = 0) the update's contribution to
+ * dg is the two-sided mean derivative and its contribution to dv is 0.    */
+int diffopt_rmsprop_bwd(const float* dparams_out, const float* dnu_out,
+                        const float* dmom_out, const float* grad,
+                        const float* nu, int64_t n, double lr, double alpha,
+                        double eps, double eps_root, double momentum,
+                        float* dgrad, float* dnu_in, float* dmom_in,
+                        void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,6 +1,9 @@
 """Build libdiffopt.so (the HIP library behind include/diffopt.h) for gfx950.
 
-    python -m paper_2211_06934_amd.build          # compile in-tree
+    python paper_2211_06934_amd/build.py          # compile in-tree
+
+Run it as a file (or through __graft_entry__.build()): importing the package
+loads the library, so the build must not go through the package.
 
 The shared library lands next to this file so that it travels with the
 source tree.  Extra preprocessor definitions (tile sizes, streaming loads)

@@ -31,7 +31,7 @@ class DiffoptError(RuntimeError):
 def _load_library():
     if not os.path.exists(_LIB_PATH):
         raise ImportError(
-            "libdiffopt.so is not built (%s); run `python -m paper_2211_06934_amd.build`" % _LIB_PATH)
+            "libdiffopt.so is not built (%s); run `python paper_2211_06934_amd/build.py`" % _LIB_PATH)
     lib = ctypes.CDLL(_LIB_PATH)
     vp, i64, i32, f64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double
     pp = ctypes.POINTER(ctypes.c_void_p)
@@ -53,8 +53,15 @@ def _load_library():
         "diffopt_adam_bwd_tree": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, *hyper, vp, vp, vp, vp]),
         "diffopt_adam_unrolled_fwd_tree": (ctypes.c_int, [vp, i64, vp, pp, pp, pp, vp, *hyper, vp]),
         "diffopt_adam_unrolled_bwd_tree": (ctypes.c_int, [vp, i64, vp, pp, pp, pp, pp, vp, vp, *hyper, vp]),
+        "diffopt_sgd_fwd": (ctypes.c_int, [vp, vp, vp, i64, f64, f64, i32, vp, vp, vp]),
+        "diffopt_sgd_bwd": (ctypes.c_int, [vp, vp, i64, f64, f64, i32, vp, vp, vp]),
+        "diffopt_rmsprop_fwd": (ctypes.c_int, [vp, vp, vp, vp, i64, f64, f64, f64, f64, f64, vp, vp, vp, vp]),
+        "diffopt_rmsprop_bwd": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, f64, f64, f64, f64, f64, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
+        if not hasattr(lib, name):
+            raise ImportError("%s lacks %s: it is older than its sources; rebuild with "
+                              "`python paper_2211_06934_amd/build.py`" % (_LIB_PATH, name))
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
@@ -297,3 +304,50 @@ def adam_unrolled_bwd_tree(table: SegTable, dpK, grads, mu_traj, nu_traj, dgrads
         _leaf_array_list(mu_traj[:K], "mu_traj", k), _leaf_array_list(nu_traj[:K], "nu_traj", k),
         _leaf_array_list(dgrads, "dgrads", k), _leaf_array(dmu0, "dmu0", k), _leaf_array(dnu0, "dnu0", k),
         int(count0), float(lr), float(b1), float(b2), float(eps), float(eps_root), _stream(stream)))
+
+
+# ---- SGD-momentum and RMSProp (flat fp32 buffers)
+
+
+def sgd_fwd(params, grad, trace, lr, momentum, nesterov, params_out, trace_out=None, stream=None,
+            n: Optional[int] = None) -> None:
+    """diffopt_sgd_fwd; trace may be None (zero), trace_out is needed when momentum > 0."""
+    if n is None:
+        n = params.numel()
+    _check(_lib.diffopt_sgd_fwd(_addr(params, "params", n=n), _addr(grad, "grad", n=n),
+                                _addr(trace, "trace", n=n), int(n), float(lr), float(momentum),
+                                int(bool(nesterov)), _addr(params_out, "params_out", n=n),
+                                _addr(trace_out, "trace_out", n=n), _stream(stream)))
+
+
+def sgd_bwd(dparams_out, dtrace_out, lr, momentum, nesterov, dgrad, dtrace_in=None, stream=None,
+            n: Optional[int] = None) -> None:
+    """diffopt_sgd_bwd; dtrace_out may be None (zero)."""
+    if n is None:
+        n = dparams_out.numel()
+    _check(_lib.diffopt_sgd_bwd(_addr(dparams_out, "dparams_out", n=n), _addr(dtrace_out, "dtrace_out", n=n),
+                                int(n), float(lr), float(momentum), int(bool(nesterov)),
+                                _addr(dgrad, "dgrad", n=n), _addr(dtrace_in, "dtrace_in", n=n), _stream(stream)))
+
+
+def rmsprop_fwd(params, grad, nu, mom, lr, alpha, eps, eps_root, momentum, params_out, nu_out, mom_out=None,
+                stream=None, n: Optional[int] = None) -> None:
+    """diffopt_rmsprop_fwd; mom may be None (zero), mom_out is needed when momentum > 0."""
+    if n is None:
+        n = params.numel()
+    _check(_lib.diffopt_rmsprop_fwd(_addr(params, "params", n=n), _addr(grad, "grad", n=n), _addr(nu, "nu", n=n),
+                                    _addr(mom, "mom", n=n), int(n), float(lr), float(alpha), float(eps),
+                                    float(eps_root), float(momentum), _addr(params_out, "params_out", n=n),
+                                    _addr(nu_out, "nu_out", n=n), _addr(mom_out, "mom_out", n=n), _stream(stream)))
+
+
+def rmsprop_bwd(dparams_out, dnu_out, dmom_out, grad, nu, lr, alpha, eps, eps_root, momentum, dgrad, dnu_in,
+                dmom_in=None, stream=None, n: Optional[int] = None) -> None:
+    """diffopt_rmsprop_bwd; dnu_out / dmom_out may be None (zero)."""
+    if n is None:
+        n = dparams_out.numel()
+    _check(_lib.diffopt_rmsprop_bwd(_addr(dparams_out, "dparams_out", n=n), _addr(dnu_out, "dnu_out", n=n),
+                                    _addr(dmom_out, "dmom_out", n=n), _addr(grad, "grad", n=n),
+                                    _addr(nu, "nu", n=n), int(n), float(lr), float(alpha), float(eps),
+                                    float(eps_root), float(momentum), _addr(dgrad, "dgrad", n=n),
+                                    _addr(dnu_in, "dnu_in", n=n), _addr(dmom_in, "dmom_in", n=n), _stream(stream)))
