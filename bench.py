@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="many_small",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
-                             "many_small_treemap", "sgd_flat", "rmsprop_flat"])
+                             "many_small_treemap", "sgd_flat", "rmsprop_flat", "es_resnet18"])
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time replays (no per-phase split)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -67,6 +67,7 @@ KERNEL_SOURCES = {  # the sources each kernel family is built from
     "sgd_fwd": ("optim.hip", "adam_math.hpp", "common.hpp"), "sgd_bwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
     "rmsprop_fwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
     "rmsprop_bwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
+    "es_perturb": ("es.hip", "adam_math.hpp", "common.hpp"), "es_estimate": ("es.hip", "adam_math.hpp", "common.hpp"),
 }
 
 
@@ -292,6 +293,37 @@ def phases_optim(S):
     return [("rmsprop_fwd", "rmsprop_fwd", 1, 28 * n), ("rmsprop_bwd", "rmsprop_bwd", 1, 32 * n)]
 
 
+def setup_es(torch, P, w):
+    """Zero-order (ES) estimation for the ResNet-18 parameter count: 64
+    antithetic noise rows, the perturbed points, and the weighted reduction
+    (the weights stand in for the caller's evaluations)."""
+    from workloads import torch_normal
+    n, N, dev = w.n, 64, "cuda"
+    S = dict(K=1, n=n, N=N, sigma=0.05, theta=torch_normal(n, 0.05, 401, dev),
+             noise=torch_normal(N * n, 1.0, 402, dev).reshape(N, n),
+             pts=torch.empty(2 * N, n, device=dev), w=torch_normal(N, 1.0, 403, dev),
+             grad=torch.empty(n, device=dev))
+    return S
+
+
+def step_es(P, S, ev=None):
+    if ev:
+        ev[0].record()
+    P.es_perturb(S["theta"], S["noise"], S["sigma"], True, S["pts"])
+    if ev:
+        ev[1].record()
+    P.es_estimate(S["noise"], S["w"], 1.0 / (2 * S["N"] * S["sigma"]), S["grad"])
+    if ev:
+        ev[2].record()
+
+
+def phases_es(S):
+    n, N = S["n"], S["N"]
+    # perturb: theta once + N noise rows in, 2N points out; estimate: N rows in, grad out
+    return [("es_perturb", "es_perturb", 1, 4 * n + 4 * N * n + 8 * N * n),
+            ("es_estimate", "es_estimate", 1, 4 * N * n + 4 * n)]
+
+
 def phases_flat_1b(S):
     n = S["n"]
     return [("adam_fwd", "adam_fwd", 1, B_FWD * n), ("adam_bwd", "adam_bwd", 1, B_BWD * n)]
@@ -397,9 +429,11 @@ def main():
     if not torch.cuda.is_available():
         sys.stderr.write("bench.py: no GPU visible\n")
         sys.exit(1)
-    w = WORKLOADS["many_small" if a.workload in ("many_small_treemap", "sgd_flat", "rmsprop_flat")
-                  else a.workload]()
-    if a.workload in ("sgd_flat", "rmsprop_flat"):
+    w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
+                   "es_resnet18": "resnet18_k1"}.get(a.workload, a.workload)]()
+    if a.workload == "es_resnet18":
+        S, step, phases = setup_es(torch, P, w), step_es, phases_es
+    elif a.workload in ("sgd_flat", "rmsprop_flat"):
         S, step, phases = setup_optim(torch, P, a.workload.split("_")[0]), step_optim, phases_optim
     elif a.workload == "flat_1b":
         S, step, phases = setup_flat_1b(torch, P, w), step_flat_1b, phases_flat_1b
@@ -476,7 +510,7 @@ def main():
                     "avg_launch_us": round(avg_launch_s * 1e6, 2)}
 
     cpu = None
-    if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat"):
+    if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "es_resnet18"):
         cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
         cpu["value"] = float("%.4g" % cpu["value"])
 
@@ -490,6 +524,7 @@ def main():
                            "leaf-direct K=%d unrolled Adam fwd+bwd (no pack/unpack)" % K),
                        "sgd_flat": "flat fp32 buffer, n=%d, one Nesterov SGD-momentum fwd + bwd" % n,
                        "rmsprop_flat": "flat fp32 buffer, n=%d, one RMSProp-momentum fwd + bwd" % n,
+                       "es_resnet18": "ES gradient estimate for n=%d (ResNet-18 size), 64 antithetic samples" % n,
                    }.get(a.workload, w.description),
                    "n_params": n, "leaves": w.nseg, "K": K,
                    "step": {"flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",

@@ -304,6 +304,34 @@ int diffopt_rmsprop_bwd(const float* dparams_out, const float* dnu_out,
                         float* dgrad, float* dnu_in, float* dmom_in,
                         void* stream);
 
+/* -------------------------------------------------------------------------
+ * Zero-order (evolution-strategies) gradient estimation (Sec. 2.2
+ * "Zero-order Differentiation"): grad f_s(theta) = (1/s) E_z[f(theta + s z) z]
+ * for the Gaussian smoothing f_s(theta) = E_z[f(theta + s z)], z ~ N(0, I),
+ * estimated by Monte-Carlo over N noise vectors that the caller draws.
+ *
+ * es_perturb: the points at which the caller evaluates f.
+ *   params      theta [n]
+ *   noise       [num_samples][n], row-major (row i is z_i)
+ *   out         [num_samples][n], row i = theta + sigma z_i; with antithetic != 0
+ *               [2 num_samples][n], rows num_samples + i = theta - sigma z_i
+ * num_samples <= 524,280.  n % 4 == 0 with 16-byte aligned pointers takes
+ * 128-bit accesses; anything else an element path with the same result.    */
+int diffopt_es_perturb(const float* params, const float* noise,
+                       int64_t num_samples, int64_t n, double sigma,
+                       int32_t antithetic, float* out, void* stream);
+
+/* es_estimate: grad_j = scale * sum_i weights_i noise_ij, accumulated in
+ * sample order in fp32.  weights is a DEVICE array [num_samples] formed by the
+ * caller from its evaluations f_i:
+ *   plain:       w_i = f(theta + s z_i),                    scale = 1/(N s)
+ *   baseline:    w_i = f(theta + s z_i) - f(theta),         scale = 1/(N s)
+ *   antithetic:  w_i = f(theta + s z_i) - f(theta - s z_i), scale = 1/(2 N s)
+ * num_samples == 0 writes zeros.                                            */
+int diffopt_es_estimate(const float* noise, const float* weights,
+                        int64_t num_samples, int64_t n, double scale,
+                        float* grad, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -302,3 +302,40 @@ def sgd_bwd_mag(dP, dT, lr, momentum=0.0, nesterov=False):
     mag_T = adT + (lr * momentum if nesterov else lr) * dP
     mag_dg = mag_T + (lr * dP if nesterov else 0.0)
     return mag_dg, momentum * mag_T
+
+
+def es_perturb(theta, noise, sigma, antithetic=False):
+    """Rows theta + sigma z_i (then theta - sigma z_i if antithetic), fp64 [N or 2N, n]."""
+    theta = _f64(theta)
+    n = theta.size
+    Z = np.ascontiguousarray(np.asarray(noise, dtype=np.float64).reshape(-1, n))
+    N = Z.shape[0]
+    out = np.empty(((2 if antithetic else 1) * N, n))
+    lib = _load()
+    lib.oracle_es_perturb.argtypes = [ctypes.c_int64, ctypes.c_int64] + [ctypes.POINTER(ctypes.c_double)] * 2 + \
+        [ctypes.c_double, ctypes.c_int64, ctypes.POINTER(ctypes.c_double)]
+    lib.oracle_es_perturb.restype = None
+    lib.oracle_es_perturb(N, n, _ptr(theta), _ptr(Z), float(sigma), int(bool(antithetic)), _ptr(out))
+    return out
+
+
+def es_estimate(noise, weights, scale):
+    """grad = scale * sum_i w_i z_i (sample order), fp64 [n]."""
+    w = _f64(weights)
+    N = w.size
+    Z = np.ascontiguousarray(np.asarray(noise, dtype=np.float64).reshape(N, -1))
+    n = Z.shape[1]
+    g = np.empty(n)
+    lib = _load()
+    lib.oracle_es_estimate.argtypes = [ctypes.c_int64, ctypes.c_int64] + [ctypes.POINTER(ctypes.c_double)] * 2 + \
+        [ctypes.c_double, ctypes.POINTER(ctypes.c_double)]
+    lib.oracle_es_estimate.restype = None
+    lib.oracle_es_estimate(N, n, _ptr(Z), _ptr(w), float(scale), _ptr(g))
+    return g
+
+
+def es_estimate_mag(noise, weights, scale):
+    """Tolerance scale of es_estimate: |scale| * sum_i |w_i z_ij|."""
+    w = np.abs(_f64(weights))
+    Z = np.abs(np.asarray(noise, dtype=np.float64).reshape(w.size, -1))
+    return abs(scale) * (w @ Z)

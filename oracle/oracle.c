@@ -416,3 +416,34 @@ void oracle_rmsprop_bwd_mag(int64_t n, const double* dP, const double* dV, const
     if (mag_db) mag_db[i] = mu * aBt;
   }
 }
+
+/* ---------------------------------------------------------------------------
+ * Zero-order (evolution-strategies) gradient estimation (Sec. 2.2 "Zero-order
+ * Differentiation"): the gradient of the Gaussian smoothing
+ * f_s(theta) = E_z[f(theta + s z)], z ~ N(0, I), is (1/s) E_z[f(theta + s z) z].
+ * Monte-Carlo with N given noise vectors z_1..z_N (rows of `noise`, N x n):
+ *
+ * es_perturb: the points to evaluate, row i of out = theta + s z_i; with
+ *   antithetic sampling also row N + i = theta - s z_i (out has 2N rows).
+ */
+void oracle_es_perturb(int64_t N, int64_t n, const double* theta, const double* noise, double sigma,
+                       int64_t antithetic, double* out) {
+  for (int64_t i = 0; i < N; ++i)
+    for (int64_t j = 0; j < n; ++j) {
+      out[i * n + j] = theta[j] + sigma * noise[i * n + j];
+      if (antithetic) out[(N + i) * n + j] = theta[j] - sigma * noise[i * n + j];
+    }
+}
+
+/* es_estimate: grad_j = scale * sum_i w_i z_ij, summed in sample order.  The
+ * caller forms the weights from the evaluated values f_i:
+ *   plain:       w_i = f(theta + s z_i),                         scale = 1/(N s)
+ *   baseline:    w_i = f(theta + s z_i) - f(theta),              scale = 1/(N s)
+ *   antithetic:  w_i = f(theta + s z_i) - f(theta - s z_i),      scale = 1/(2 N s) */
+void oracle_es_estimate(int64_t N, int64_t n, const double* noise, const double* w, double scale, double* grad) {
+  for (int64_t j = 0; j < n; ++j) {
+    double acc = 0.0;
+    for (int64_t i = 0; i < N; ++i) acc += w[i] * noise[i * n + j];
+    grad[j] = scale * acc;
+  }
+}

@@ -13,7 +13,7 @@ from .diffopt import (DiffoptError, SegTable, adam_bwd, adam_bwd_tree, adam_fwd,
                       adam_unrolled_bwd, adam_unrolled_bwd_tree, adam_unrolled_fwd,
                       adam_unrolled_fwd_tree, last_error, segtable_create, segtable_destroy,
                       segtable_nseg, segtable_total, tree_flatten, tree_unflatten,
-                      sgd_fwd, sgd_bwd, rmsprop_fwd, rmsprop_bwd)
+                      sgd_fwd, sgd_bwd, rmsprop_fwd, rmsprop_bwd, es_perturb, es_estimate)
 from . import tree
 from . import autograd
 from .autograd import AdamFn, AdamHyper, AdamState, AdamTreeFn, FlatAdam, MetaAdam
@@ -21,7 +21,8 @@ from .autograd import AdamFn, AdamHyper, AdamState, AdamTreeFn, FlatAdam, MetaAd
 __all__ = [
     "diffopt", "tree", "autograd", "DiffoptError", "SegTable", "adam_bwd", "adam_fwd",
     "adam_unrolled_bwd", "adam_unrolled_fwd", "adam_fwd_tree", "adam_bwd_tree",
-    "adam_unrolled_fwd_tree", "adam_unrolled_bwd_tree", "sgd_fwd", "sgd_bwd", "rmsprop_fwd", "rmsprop_bwd", "last_error", "segtable_create", "segtable_destroy",
+    "adam_unrolled_fwd_tree", "adam_unrolled_bwd_tree", "sgd_fwd", "sgd_bwd", "rmsprop_fwd", "rmsprop_bwd",
+    "es_perturb", "es_estimate", "last_error", "segtable_create", "segtable_destroy",
     "segtable_nseg", "segtable_total", "tree_flatten", "tree_unflatten", "AdamFn", "AdamHyper",
     "AdamState", "FlatAdam", "AdamTreeFn", "MetaAdam",
 ]

@@ -181,3 +181,50 @@ class MetaAdam:
             self._set(name, torch.nn.Parameter(p.detach().clone()) if not isinstance(p, torch.nn.Parameter) else p)
         self.mu = [m.detach() for m in self.mu]
         self.nu = [v.detach() for v in self.nu]
+
+
+def es_gradient(fn, theta: torch.Tensor, sigma: float, num_samples: int, method: str = "antithetic",
+                generator: torch.Generator = None) -> torch.Tensor:
+    """Zero-order (ES) estimate of the gradient of the Gaussian smoothing of fn
+    at theta (Sec. 2.2): draws N(0, I) noise with the caller's generator,
+    builds the perturbed points with diffopt_es_perturb, evaluates fn on them
+    as one batch (fn maps [M, n] to [M]) and reduces with diffopt_es_estimate.
+    method: "plain", "baseline" (subtract f(theta)) or "antithetic"."""
+    if method not in ("plain", "baseline", "antithetic"):
+        raise ValueError("method must be plain, baseline or antithetic")
+    theta = theta.detach().contiguous().reshape(-1)
+    n = theta.numel()
+    noise = torch.randn(num_samples, n, device=theta.device, dtype=theta.dtype, generator=generator)
+    anti = method == "antithetic"
+    pts = torch.empty((2 if anti else 1) * num_samples, n, device=theta.device, dtype=theta.dtype)
+    _d.es_perturb(theta, noise, sigma, anti, pts)
+    with torch.no_grad():
+        fv = fn(pts).reshape(-1).to(theta.dtype)
+        if method == "plain":
+            w, scale = fv, 1.0 / (num_samples * sigma)
+        elif method == "baseline":
+            w, scale = fv - fn(theta.reshape(1, -1)).reshape(()), 1.0 / (num_samples * sigma)
+        else:
+            w, scale = fv[:num_samples] - fv[num_samples:], 1.0 / (2 * num_samples * sigma)
+    grad = torch.empty_like(theta)
+    _d.es_estimate(noise, w.contiguous(), scale, grad)
+    return grad
+
+
+class ZeroOrderFn(torch.autograd.Function):
+    """y = fn(theta) whose backward is the ES gradient estimate (Sec. 2.2,
+    the zero_order decorator's behaviour): grad_theta = grad_y * estimate."""
+
+    @staticmethod
+    def forward(ctx, theta, fn, sigma, num_samples, method, generator):
+        ctx.save_for_backward(theta)
+        ctx.cfg = (fn, sigma, num_samples, method, generator)
+        with torch.no_grad():
+            return fn(theta.detach().reshape(1, -1)).reshape(())
+
+    @staticmethod
+    def backward(ctx, grad_y):
+        (theta,) = ctx.saved_tensors
+        fn, sigma, num_samples, method, generator = ctx.cfg
+        g = es_gradient(fn, theta, sigma, num_samples, method, generator).reshape(theta.shape)
+        return grad_y * g, None, None, None, None, None

@@ -57,6 +57,8 @@ def _load_library():
         "diffopt_sgd_bwd": (ctypes.c_int, [vp, vp, i64, f64, f64, i32, vp, vp, vp]),
         "diffopt_rmsprop_fwd": (ctypes.c_int, [vp, vp, vp, vp, i64, f64, f64, f64, f64, f64, vp, vp, vp, vp]),
         "diffopt_rmsprop_bwd": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, f64, f64, f64, f64, f64, vp, vp, vp, vp]),
+        "diffopt_es_perturb": (ctypes.c_int, [vp, vp, i64, i64, f64, i32, vp, vp]),
+        "diffopt_es_estimate": (ctypes.c_int, [vp, vp, i64, i64, f64, vp, vp]),
     }
     for name, (res, args) in sig.items():
         if not hasattr(lib, name):
@@ -351,3 +353,26 @@ def rmsprop_bwd(dparams_out, dnu_out, dmom_out, grad, nu, lr, alpha, eps, eps_ro
                                     _addr(nu, "nu", n=n), int(n), float(lr), float(alpha), float(eps),
                                     float(eps_root), float(momentum), _addr(dgrad, "dgrad", n=n),
                                     _addr(dnu_in, "dnu_in", n=n), _addr(dmom_in, "dmom_in", n=n), _stream(stream)))
+
+
+# ---- zero-order (ES) gradient estimation
+
+
+def es_perturb(params, noise, sigma, antithetic, out, stream=None) -> None:
+    """diffopt_es_perturb: noise is [N, n]; out is [N, n] (or [2N, n] if antithetic)."""
+    n = params.numel()
+    N = noise.numel() // n if n else 0
+    if noise.numel() != N * n or out.numel() != (2 if antithetic else 1) * N * n:
+        raise ValueError("noise must be [N, n] and out [N or 2N, n]")
+    _check(_lib.diffopt_es_perturb(_addr(params, "params"), _addr(noise, "noise"), int(N), int(n), float(sigma),
+                                   int(bool(antithetic)), _addr(out, "out"), _stream(stream)))
+
+
+def es_estimate(noise, weights, scale, grad, stream=None) -> None:
+    """diffopt_es_estimate: grad = scale * weights @ noise (noise [N, n], weights [N] on the device)."""
+    n = grad.numel()
+    N = weights.numel()
+    if noise.numel() != N * n:
+        raise ValueError("noise must be [N, n] with N = weights.numel(), n = grad.numel()")
+    _check(_lib.diffopt_es_estimate(_addr(noise, "noise"), _addr(weights, "weights"), int(N), int(n), float(scale),
+                                    _addr(grad, "grad"), _stream(stream)))
