@@ -2,8 +2,9 @@
 
 One step = one pass of the whole path over one batch of synthetic input:
   tree flatten of the params tree and of K gradient trees
-  -> K-step unrolled Adam forward (K fused fwd kernels, trajectory kept)
-  -> K-step unrolled Adam backward (K fused VJP kernels, meta-gradient)
+  -> K-step unrolled Adam forward (the K steps fused in one kernel per 16
+     steps, running params in registers, trajectory kept)
+  -> K-step unrolled Adam backward (the same, running cotangents in registers)
   -> tree unflatten of p_K and of the K gradient cotangents.
 Default workload: the many-small-tensor tree (20,000 fp32 leaves, log-uniform
 sizes in [1, 65536], K = 3).  All inputs are resident in HBM before timing.
@@ -40,6 +41,17 @@ B_FWD = 28          # p, g, m, v -> p', m', v'
 B_BWD = 36          # dP, dM, dV, g, m, v -> dg, dm, dv
 B_BWD_FIRST = 28    # dM = dV = 0: dP, g, m, v -> dg, dm, dv
 B_COPY = 8          # pack / unpack: read once, write once
+UNROLL_CHUNK = 16   # steps per launch of the fused K-step driver
+
+
+def b_unrolled_fwd(K):
+    """K fused forward steps: p0, mu0, nu0 and K gradients in; K (mu, nu) and p_K out."""
+    return 16 + 12 * K
+
+
+def b_unrolled_bwd(K):
+    """K fused backward steps: dp_K and K (g, mu, nu) in; K dg and dmu0, dnu0 out."""
+    return 12 + 16 * K
 
 
 def parse():
@@ -60,6 +72,8 @@ def parse():
 KERNEL_SOURCES = {  # the sources each kernel family is built from
     "adam_fwd": ("adam.hip", "adam_math.hpp", "common.hpp"),
     "adam_bwd": ("adam.hip", "adam_math.hpp", "common.hpp"),
+    "adam_unrolled_fwd": ("adam.hip", "adam_math.hpp", "common.hpp"),
+    "adam_unrolled_bwd": ("adam.hip", "adam_math.hpp", "common.hpp"),
     "tree_flatten": ("tree.hip", "segtable.hpp", "common.hpp"),
     "tree_unflatten": ("tree.hip", "segtable.hpp", "common.hpp"),
     "adam_fwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
@@ -163,8 +177,8 @@ def phases_tree(S):
     K, n = S["K"], S["n"]
     return [
         ("flatten", "tree_flatten", K + 1, (K + 1) * B_COPY * n),
-        ("adam_fwd", "adam_fwd", K, K * B_FWD * n),
-        ("adam_bwd", "adam_bwd", K, (B_BWD_FIRST + (K - 1) * B_BWD) * n),
+        ("adam_fwd", "adam_unrolled_fwd", -(-K // UNROLL_CHUNK), b_unrolled_fwd(K) * n),
+        ("adam_bwd", "adam_unrolled_bwd", -(-K // UNROLL_CHUNK), b_unrolled_bwd(K) * n),
         ("unflatten", "tree_unflatten", K + 1, (K + 1) * B_COPY * n),
     ]
 

@@ -165,9 +165,14 @@ int diffopt_adam_bwd(const float* dupdate, const float* dmu, const float* dnu,
  *               read, mu_traj[k] receives mu_k (the trajectory the backward
  *               needs); all K+1 buffers distinct
  *   nu_traj     the same for nu
- *   pK          output [n]; also the running params buffer (steps 2..K
- *               update it in place)
- * Enqueues K kernels on `stream`, no host synchronisation.                  */
+ *   pK          output [n] (may equal p0)
+ * grads, mu_traj[1..K], nu_traj[1..K] and pK must not overlap one another or
+ * p0, mu_traj[0], nu_traj[0] (pK == p0 excepted).
+ * The K steps run fused, one kernel per 16 steps: each element's running
+ * params stay in registers between steps, so K steps move 16 + 12K bytes per
+ * element.  The result equals K calls of diffopt_adam_fwd bit for bit.  With
+ * any pointer not 16-byte aligned it enqueues K single-step kernels instead
+ * (same result).  No host synchronisation.                                  */
 int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0,
                               const float* const* grads,
                               float* const* mu_traj, float* const* nu_traj,
@@ -186,9 +191,14 @@ int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0,
  *               arrays of device pointers; mu_traj[K], nu_traj[K] unused)
  *   dgrads      HOST array [K] of device pointers: dgrads[k-1] receives the
  *               cotangent of g_k
- *   dmu0, dnu0  outputs [n]: cotangents of mu0, nu0 (used as the running
- *               dM, dV buffers, updated in place)
- * Enqueues K kernels on `stream`, the first with zero dM, dV.               */
+ *   dmu0, dnu0  outputs [n]: cotangents of mu0, nu0 (also the running dM,
+ *               dV between launches when K > 16)
+ * Outputs must not overlap the inputs or one another.
+ * The K steps run fused, last step first, one kernel per 16 steps: each
+ * element's dM, dV stay in registers, so K steps move 12 + 16K bytes per
+ * element.  The result equals K calls of diffopt_adam_bwd (the first with
+ * zero dM, dV) bit for bit.  With any pointer not 16-byte aligned it
+ * enqueues those K single-step kernels instead.                             */
 int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
                               const float* const* grads,
                               const float* const* mu_traj,

@@ -26,6 +26,9 @@
 #ifndef DIFFOPT_ADAM_BLOCK
 #define DIFFOPT_ADAM_BLOCK 1024  // threads per workgroup of the Adam kernels
 #endif
+#ifndef DIFFOPT_UNROLL_BLOCK
+#define DIFFOPT_UNROLL_BLOCK 256  // threads per workgroup of the fused K-step kernels
+#endif
 
 namespace diffopt {
 
@@ -236,6 +239,190 @@ __global__ __launch_bounds__(kAB) void adam_bwd_scalar(const float* dP, const fl
   }
 }
 
+// ---- fused K-step unrolled kernels -----------------------------------------------
+// One launch runs up to kUK consecutive steps of the unrolled loop for every
+// element it owns.  The running params (forward) and the running cotangents
+// dP, dM, dV (backward) stay in registers between steps instead of making a
+// round trip through HBM, so K steps move 16 + 12K bytes per element forward
+// (p0, mu0, nu0 and K gradients in; K mu/nu pairs and p_K out) and 12 + 16K
+// backward (dP and K (g, mu, nu) triples in; K dg and dmu0, dnu0 out), against
+// 28K and 36K - 8 for K separate step kernels.  Each step's arithmetic is the
+// same fwd_elem / bwd_elem as the single-step kernels, in the same order.
+// The next step's loads are issued before the current step's arithmetic.
+
+constexpr int kUK = 16;  // steps per fused launch (kernel-argument space bounds it)
+constexpr int kUB = DIFFOPT_UNROLL_BLOCK;
+
+// Step s of a launch is the launch's s-th step in execution order.
+struct UFwdArgs {
+  const float* p;   // params before the launch's first step
+  const float* m0;  // mu, nu before the first step
+  const float* v0;
+  float* pK;  // params after the last step
+  const float* g[kUK];
+  float* m[kUK];  // mu, nu after step s
+  float* v[kUK];
+  AdamCoef c[kUK];
+  int64_t n;
+  int32_t K;  // steps in this launch, 1..kUK
+};
+
+// Execution order of the backward is reverse step order: step s of a launch
+// is unrolled step k_hi - s, with the state (g, mu, nu) that step consumed.
+struct UBwdArgs {
+  const float* dP;  // cotangent of the final params (constant through Adam steps)
+  float* dm;        // running dM, dV: read first if init_mv, written at the end
+  float* dv;
+  const float* g[kUK];
+  const float* m[kUK];
+  const float* v[kUK];
+  float* dg[kUK];
+  AdamCoef c[kUK];
+  int64_t n;
+  int32_t K;
+  int32_t init_mv;  // 0: dM = dV = 0 before the first step (the last unrolled step)
+};
+
+__device__ __forceinline__ const f32x4* cv4(const float* q) { return reinterpret_cast<const f32x4*>(q); }
+__device__ __forceinline__ f32x4* v4(float* q) { return reinterpret_cast<f32x4*>(q); }
+
+__device__ __forceinline__ void ufwd_vector(int64_t i, const UFwdArgs& a) {
+  f32x4 P = ld(cv4(a.p) + i), M = ld(cv4(a.m0) + i), V = ld(cv4(a.v0) + i);
+  f32x4 G = ld(cv4(a.g[0]) + i);
+  for (int s = 0; s < a.K; ++s) {  // a runtime loop keeps the code small
+    f32x4 Gn = G;
+    if (s + 1 < a.K) Gn = ld(cv4(a.g[s + 1]) + i);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const FwdOut o = fwd_elem(P[e], G[e], M[e], V[e], a.c[s]);
+      P[e] = o.p;
+      M[e] = o.m;
+      V[e] = o.v;
+    }
+    st(v4(a.m[s]) + i, M);
+    st(v4(a.v[s]) + i, V);
+    G = Gn;
+  }
+  st(v4(a.pK) + i, P);
+}
+
+__device__ __forceinline__ void ufwd_element(int64_t e, const UFwdArgs& a) {
+  float P = a.p[e], M = a.m0[e], V = a.v0[e];
+  for (int s = 0; s < a.K; ++s) {
+    const FwdOut o = fwd_elem(P, a.g[s][e], M, V, a.c[s]);
+    P = o.p;
+    M = o.m;
+    V = o.v;
+    a.m[s][e] = M;
+    a.v[s][e] = V;
+  }
+  a.pK[e] = P;
+}
+
+// Tile t covers 16-byte vectors [t B, (t+1) B) for B threads per workgroup;
+// only the last tile checks bounds, and the last workgroup also runs the
+// n % 4 tail elements.
+__global__ __launch_bounds__(kUB) void adam_unrolled_fwd_vec(UFwdArgs a) {
+  const int64_t nv = a.n >> 2;
+  const int64_t ntiles = (nv + kUB - 1) / kUB;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t i = t * kUB + threadIdx.x;
+    if (i < nv) ufwd_vector(i, a);
+  }
+  if (blockIdx.x == gridDim.x - 1) {
+    const int64_t e = (nv << 2) + threadIdx.x;
+    if (e < a.n) ufwd_element(e, a);
+  }
+}
+
+template <bool HAS_MV>
+__device__ __forceinline__ void ubwd_step(const f32x4& dP, f32x4& dM, f32x4& dV, const f32x4& g, const f32x4& m,
+                                          const f32x4& v, const AdamCoef& c, f32x4* dgo) {
+  f32x4 rg;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const BwdOut o = bwd_elem<HAS_MV>(dP[e], dM[e], dV[e], g[e], m[e], v[e], c);
+    rg[e] = o.g;
+    dM[e] = o.m;
+    dV[e] = o.v;
+  }
+  st(dgo, rg);
+}
+
+__device__ __forceinline__ void ubwd_vector(int64_t i, const UBwdArgs& a) {
+  const f32x4 dP = ld(cv4(a.dP) + i);
+  f32x4 dM = {0.0f, 0.0f, 0.0f, 0.0f}, dV = {0.0f, 0.0f, 0.0f, 0.0f};
+  f32x4 G = ld(cv4(a.g[0]) + i), M = ld(cv4(a.m[0]) + i), V = ld(cv4(a.v[0]) + i);
+  int s = 0;
+  if (a.init_mv) {
+    dM = ld(cv4(a.dm) + i);
+    dV = ld(cv4(a.dv) + i);
+  } else {  // the last unrolled step: zero cotangents of its mu, nu outputs
+    f32x4 Gn = G, Mn = M, Vn = V;
+    if (1 < a.K) {
+      Gn = ld(cv4(a.g[1]) + i);
+      Mn = ld(cv4(a.m[1]) + i);
+      Vn = ld(cv4(a.v[1]) + i);
+    }
+    ubwd_step<false>(dP, dM, dV, G, M, V, a.c[0], v4(a.dg[0]) + i);
+    G = Gn;
+    M = Mn;
+    V = Vn;
+    s = 1;
+  }
+  for (; s < a.K; ++s) {  // a runtime loop keeps the code small
+    f32x4 Gn = G, Mn = M, Vn = V;
+    if (s + 1 < a.K) {
+      Gn = ld(cv4(a.g[s + 1]) + i);
+      Mn = ld(cv4(a.m[s + 1]) + i);
+      Vn = ld(cv4(a.v[s + 1]) + i);
+    }
+    ubwd_step<true>(dP, dM, dV, G, M, V, a.c[s], v4(a.dg[s]) + i);
+    G = Gn;
+    M = Mn;
+    V = Vn;
+  }
+  st(v4(a.dm) + i, dM);
+  st(v4(a.dv) + i, dV);
+}
+
+__device__ __forceinline__ void ubwd_element(int64_t e, const UBwdArgs& a) {
+  const float dP = a.dP[e];
+  float dM = 0.0f, dV = 0.0f;
+  int s = 0;
+  if (a.init_mv) {
+    dM = a.dm[e];
+    dV = a.dv[e];
+  } else {
+    const BwdOut o = bwd_elem<false>(dP, 0.0f, 0.0f, a.g[0][e], a.m[0][e], a.v[0][e], a.c[0]);
+    a.dg[0][e] = o.g;
+    dM = o.m;
+    dV = o.v;
+    s = 1;
+  }
+  for (; s < a.K; ++s) {
+    const BwdOut o = bwd_elem<true>(dP, dM, dV, a.g[s][e], a.m[s][e], a.v[s][e], a.c[s]);
+    a.dg[s][e] = o.g;
+    dM = o.m;
+    dV = o.v;
+  }
+  a.dm[e] = dM;
+  a.dv[e] = dV;
+}
+
+__global__ __launch_bounds__(kUB) void adam_unrolled_bwd_vec(UBwdArgs a) {
+  const int64_t nv = a.n >> 2;
+  const int64_t ntiles = (nv + kUB - 1) / kUB;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t i = t * kUB + threadIdx.x;
+    if (i < nv) ubwd_vector(i, a);
+  }
+  if (blockIdx.x == gridDim.x - 1) {
+    const int64_t e = (nv << 2) + threadIdx.x;
+    if (e < a.n) ubwd_element(e, a);
+  }
+}
+
 // ---- host launchers ------------------------------------------------------------
 
 inline bool aligned16(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -371,7 +558,36 @@ extern "C" int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0, 
     if (k < K && !grads[k]) return fail(DIFFOPT_EINVAL, "%s: null grads entry %lld", who, (long long)k);
   }
   hipStream_t st = as_stream(stream);
-  for (int64_t k = 1; k <= K; ++k) {
+  bool vec = aligned16(p0) && aligned16(pK);
+  for (int64_t k = 0; k <= K; ++k) {
+    vec = vec && aligned16(mu_traj[k]) && aligned16(nu_traj[k]);
+    if (k < K) vec = vec && aligned16(grads[k]);
+  }
+  if (vec) {  // fused: one launch per kUK steps
+    for (int64_t k0 = 0; k0 < K; k0 += kUK) {
+      UFwdArgs a;
+      a.K = (int32_t)(K - k0 < kUK ? K - k0 : kUK);
+      a.n = n;
+      a.p = (k0 == 0) ? p0 : pK;
+      a.m0 = mu_traj[k0];
+      a.v0 = nu_traj[k0];
+      a.pK = pK;
+      for (int s = 0; s < kUK; ++s) {
+        const bool on = s < a.K;
+        a.g[s] = on ? grads[k0 + s] : nullptr;
+        a.m[s] = on ? mu_traj[k0 + s + 1] : nullptr;
+        a.v[s] = on ? nu_traj[k0 + s + 1] : nullptr;
+        if (on) make_coef(who, count0 + k0 + s, lr, b1, b2, eps, eps_root, &a.c[s]);
+        else a.c[s] = AdamCoef{};
+      }
+      const int64_t blocks = grid_for(((n >> 2) + kUB - 1) / kUB);
+      hipLaunchKernelGGL(adam_unrolled_fwd_vec, dim3((unsigned)blocks), dim3(kUB), 0, st, a);
+      int rc = launch_status(who);
+      if (rc) return rc;
+    }
+    return DIFFOPT_OK;
+  }
+  for (int64_t k = 1; k <= K; ++k) {  // any pointer not 16-byte aligned: step by step
     make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &c);
     const float* src = (k == 1) ? p0 : pK;
     int rc = launch_fwd(src, grads[k - 1], mu_traj[k - 1], nu_traj[k - 1], n, c, pK, mu_traj[k], nu_traj[k],
@@ -403,7 +619,36 @@ extern "C" int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
       return fail(DIFFOPT_EINVAL, "%s: null entry %lld in a pointer array", who, (long long)k);
   }
   hipStream_t st = as_stream(stream);
-  for (int64_t k = K; k >= 1; --k) {
+  bool vec = aligned16(dpK) && aligned16(dmu0) && aligned16(dnu0);
+  for (int64_t k = 0; k < K; ++k)
+    vec = vec && aligned16(grads[k]) && aligned16(mu_traj[k]) && aligned16(nu_traj[k]) && aligned16(dgrads[k]);
+  if (vec) {  // fused: one launch per kUK steps, last steps first
+    for (int64_t khi = K; khi >= 1; khi -= kUK) {
+      UBwdArgs a;
+      a.K = (int32_t)(khi < kUK ? khi : kUK);
+      a.n = n;
+      a.dP = dpK;
+      a.dm = dmu0;
+      a.dv = dnu0;
+      a.init_mv = khi != K;  // the first launch starts from zero cotangents of mu_K, nu_K
+      for (int s = 0; s < kUK; ++s) {
+        const bool on = s < a.K;
+        const int64_t k = khi - s;  // unrolled step (1-based) run as the launch's step s
+        a.g[s] = on ? grads[k - 1] : nullptr;
+        a.m[s] = on ? mu_traj[k - 1] : nullptr;
+        a.v[s] = on ? nu_traj[k - 1] : nullptr;
+        a.dg[s] = on ? dgrads[k - 1] : nullptr;
+        if (on) make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &a.c[s]);
+        else a.c[s] = AdamCoef{};
+      }
+      const int64_t blocks = grid_for(((n >> 2) + kUB - 1) / kUB);
+      hipLaunchKernelGGL(adam_unrolled_bwd_vec, dim3((unsigned)blocks), dim3(kUB), 0, st, a);
+      int rc = launch_status(who);
+      if (rc) return rc;
+    }
+    return DIFFOPT_OK;
+  }
+  for (int64_t k = K; k >= 1; --k) {  // any pointer not 16-byte aligned: step by step
     make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &c);
     const bool first = (k == K);  // zero cotangents of mu_K, nu_K
     int rc = launch_bwd(dpK, first ? nullptr : dmu0, first ? nullptr : dnu0, grads[k - 1], mu_traj[k - 1],
