@@ -42,6 +42,7 @@ B_BWD = 36          # dP, dM, dV, g, m, v -> dg, dm, dv
 B_BWD_FIRST = 28    # dM = dV = 0: dP, g, m, v -> dg, dm, dv
 B_COPY = 8          # pack / unpack: read once, write once
 UNROLL_CHUNK = 16   # steps per launch of the fused K-step driver
+TREE_UNROLL_CHUNK = 8  # the same for its leaf-direct form
 
 
 def b_unrolled_fwd(K):
@@ -78,6 +79,8 @@ KERNEL_SOURCES = {  # the sources each kernel family is built from
     "tree_unflatten": ("tree.hip", "segtable.hpp", "common.hpp"),
     "adam_fwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
     "adam_bwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
+    "adam_unrolled_fwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
+    "adam_unrolled_bwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
     "sgd_fwd": ("optim.hip", "adam_math.hpp", "common.hpp"), "sgd_bwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
     "rmsprop_fwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
     "rmsprop_bwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
@@ -232,8 +235,8 @@ def step_treemap(P, S, ev=None):
 
 def phases_treemap(S):
     K, n = S["K"], S["n"]
-    return [("adam_fwd_tree", "adam_fwd_tree", K, K * B_FWD * n),
-            ("adam_bwd_tree", "adam_bwd_tree", K, (B_BWD_FIRST + (K - 1) * B_BWD) * n)]
+    return [("adam_fwd_tree", "adam_unrolled_fwd_tree", -(-K // TREE_UNROLL_CHUNK), b_unrolled_fwd(K) * n),
+            ("adam_bwd_tree", "adam_unrolled_bwd_tree", -(-K // TREE_UNROLL_CHUNK), b_unrolled_bwd(K) * n)]
 
 
 def setup_flat_1b(torch, P, w):

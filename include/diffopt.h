@@ -244,8 +244,13 @@ int diffopt_adam_bwd_tree(const diffopt_segtable* table, const uint64_t* dupdate
 /* K-step unrolled driver in leaf-direct form: the recurrences of
  * diffopt_adam_unrolled_fwd / _bwd with every flat buffer replaced by a tree
  * (a device array of leaf addresses).  grads, mu_traj, nu_traj and dgrads are
- * HOST arrays ([K], [K+1], [K+1], [K]) of such device arrays; pK is also the
- * running params tree, dmu0 / dnu0 the running cotangent trees.              */
+ * HOST arrays ([K], [K+1], [K+1], [K]) of such device arrays.  The steps run
+ * fused, one kernel per 8 steps, each lane keeping its elements' running
+ * params (forward) or dM, dV (backward) in registers: 16 + 12K and 12 + 16K
+ * bytes per element, and results equal to K calls of the single-step
+ * leaf-direct entry points bit for bit.  pK may be p0; dmu0 / dnu0 also carry
+ * the running cotangents between launches when K > 8.  Output leaves must
+ * not overlap input leaves or one another.                                  */
 int diffopt_adam_unrolled_fwd_tree(const diffopt_segtable* table, int64_t K,
                                    const uint64_t* p0,
                                    const uint64_t* const* grads,

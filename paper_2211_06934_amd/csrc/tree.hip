@@ -278,8 +278,8 @@ extern "C" int diffopt_segtable_create(int64_t nseg, const int64_t* numel, const
 
 extern "C" void diffopt_segtable_destroy(diffopt_segtable* t) {
   if (!t) return;
-  if (t->d_seg) hipFree(t->d_seg);
-  if (t->d_tile_first) hipFree(t->d_tile_first);
+  if (t->d_seg) (void)hipFree(t->d_seg);  // nothing to report to: destroy has no error return
+  if (t->d_tile_first) (void)hipFree(t->d_tile_first);
   delete t;
 }
 

@@ -231,6 +231,200 @@ __global__ __launch_bounds__(kBB) void adam_bwd_tree_kernel(const SegEntry* __re
   }
 }
 
+// ---- fused K-step leaf-direct kernels ----------------------------------------------
+// The K-step driver in one launch per kTK steps, as the flat driver does it:
+// each lane finds its group once, then walks the steps with the running params
+// (forward) or dM, dV (backward) in registers, loading the next step's inputs
+// before the current step's arithmetic.  The window stages the leaf address
+// of every operand tree of every step in dynamic LDS (NA x kWindowMax x 8
+// bytes: 18.5 KiB for the backward at 8 steps).  One group per lane, one
+// table tile (512 groups) per workgroup.
+constexpr int kTK = 8;  // steps per fused launch
+constexpr int kUTB = (int)kTileGroups;
+constexpr int kTFwdNA = 4 + 3 * kTK;  // 0 p, 1 mu0, 2 nu0, 3 pK; per step s: 4+3s g, 5+3s mu_s+1, 6+3s nu_s+1
+constexpr int kTBwdNA = 3 + 4 * kTK;  // 0 dP, 1 dmu, 2 dnu; per step s: 3+4s g, 4+4s mu, 5+4s nu, 6+4s dg
+
+struct TFwdArgs {
+  const uint64_t* a[kTFwdNA];
+  AdamCoef c[kTK];
+  int32_t K;
+};
+
+// Execution order is reverse step order, as in the flat fused backward.
+struct TBwdArgs {
+  const uint64_t* a[kTBwdNA];
+  AdamCoef c[kTK];
+  int32_t K;
+  int32_t init_mv;  // 0: dM = dV = 0 before the first step
+};
+
+// Stage the window of tile b for `na` operand trees: (operand, leaf) pairs
+// are spread over the workgroup, then each leaf's all-operands-aligned flag
+// is formed from LDS.  Ends with the workgroup synchronised.
+__device__ __forceinline__ int stage_window_n(const SegEntry* __restrict__ seg, const int64_t* __restrict__ tile_first,
+                                              const uint64_t* const* arrs, int na, int dense_orig, int64_t b,
+                                              int64_t* s_goff, int64_t* s_numel, uint64_t* s_ptr, int* s_al) {
+  const int64_t j0 = tile_first[b];
+  const int W = (int)(tile_first[b + 1] - j0 + 1);
+  for (int t = threadIdx.x; t <= W; t += kUTB) {
+    const SegEntry e = seg[j0 + t];
+    s_goff[t] = e.goff;
+    if (t < W) s_numel[t] = e.numel;
+  }
+  for (int x = threadIdx.x; x < W * na; x += kUTB) {
+    const int q = x / W, t = x - q * W;
+    const int64_t leaf = dense_orig ? j0 + t : seg[j0 + t].orig;
+    s_ptr[q * kWindowMax + t] = arrs[q][leaf];
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < W; t += kUTB) {
+    uint64_t any = 0;
+    for (int q = 0; q < na; ++q) any |= s_ptr[q * kWindowMax + t];
+    s_al[t] = (any & 15u) == 0;
+  }
+  __syncthreads();
+  return W;
+}
+
+__global__ __launch_bounds__(kUTB) void adam_unrolled_fwd_tree_kernel(const SegEntry* __restrict__ seg,
+                                                                     const int64_t* __restrict__ tile_first,
+                                                                     int64_t ngroups, int dense_orig, TFwdArgs a) {
+  __shared__ int64_t s_goff[kWindowMax + 1];
+  __shared__ int64_t s_numel[kWindowMax];
+  __shared__ int s_al[kWindowMax];
+  extern __shared__ uint64_t s_ptr[];  // [na][kWindowMax]
+  const int na = 4 + 3 * a.K;
+  const int64_t b = blockIdx.x;
+  const int W = stage_window_n(seg, tile_first, a.a, na, dense_orig, b, s_goff, s_numel, s_ptr, s_al);
+  const int64_t gidx = b * kTileGroups + threadIdx.x;
+  if (gidx >= ngroups) return;
+  const int t = find_leaf(s_goff, W, gidx);
+  const int64_t e0 = 4 * (gidx - s_goff[t]);
+  const int64_t nel = s_numel[t];
+  if (e0 >= nel) return;
+  const uint64_t* P = s_ptr + t;  // P[q * kWindowMax]: leaf address in operand q
+#define OP(q) P[(q) * kWindowMax]
+  if (e0 + 4 <= nel && s_al[t]) {
+    const int64_t i = e0 >> 2;
+    f32x4 p = ld(at<const f32x4>(OP(0), i)), m = ld(at<const f32x4>(OP(1), i)), v = ld(at<const f32x4>(OP(2), i));
+    f32x4 g = ld(at<const f32x4>(OP(4), i));
+    for (int s = 0; s < a.K; ++s) {
+      f32x4 gn = g;
+      if (s + 1 < a.K) gn = ld(at<const f32x4>(OP(4 + 3 * (s + 1)), i));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const FwdOut o = fwd_elem(p[e], g[e], m[e], v[e], a.c[s]);
+        p[e] = o.p;
+        m[e] = o.m;
+        v[e] = o.v;
+      }
+      st(at<f32x4>(OP(5 + 3 * s), i), m);
+      st(at<f32x4>(OP(6 + 3 * s), i), v);
+      g = gn;
+    }
+    st(at<f32x4>(OP(3), i), p);
+  } else {
+    const int64_t end = e0 + 4 < nel ? e0 + 4 : nel;
+    for (int64_t i = e0; i < end; ++i) {
+      float p = *at<const float>(OP(0), i), m = *at<const float>(OP(1), i), v = *at<const float>(OP(2), i);
+      for (int s = 0; s < a.K; ++s) {
+        const FwdOut o = fwd_elem(p, *at<const float>(OP(4 + 3 * s), i), m, v, a.c[s]);
+        p = o.p;
+        m = o.m;
+        v = o.v;
+        *at<float>(OP(5 + 3 * s), i) = m;
+        *at<float>(OP(6 + 3 * s), i) = v;
+      }
+      *at<float>(OP(3), i) = p;
+    }
+  }
+#undef OP
+}
+
+__global__ __launch_bounds__(kUTB) void adam_unrolled_bwd_tree_kernel(const SegEntry* __restrict__ seg,
+                                                                     const int64_t* __restrict__ tile_first,
+                                                                     int64_t ngroups, int dense_orig, TBwdArgs a) {
+  __shared__ int64_t s_goff[kWindowMax + 1];
+  __shared__ int64_t s_numel[kWindowMax];
+  __shared__ int s_al[kWindowMax];
+  extern __shared__ uint64_t s_ptr[];  // [na][kWindowMax]
+  const int na = 3 + 4 * a.K;
+  const int64_t b = blockIdx.x;
+  const int W = stage_window_n(seg, tile_first, a.a, na, dense_orig, b, s_goff, s_numel, s_ptr, s_al);
+  const int64_t gidx = b * kTileGroups + threadIdx.x;
+  if (gidx >= ngroups) return;
+  const int t = find_leaf(s_goff, W, gidx);
+  const int64_t e0 = 4 * (gidx - s_goff[t]);
+  const int64_t nel = s_numel[t];
+  if (e0 >= nel) return;
+  const uint64_t* P = s_ptr + t;
+#define OP(q) P[(q) * kWindowMax]
+  if (e0 + 4 <= nel && s_al[t]) {
+    const int64_t i = e0 >> 2;
+    const f32x4 dP = ld(at<const f32x4>(OP(0), i));
+    f32x4 dM = {0.0f, 0.0f, 0.0f, 0.0f}, dV = {0.0f, 0.0f, 0.0f, 0.0f};
+    f32x4 g = ld(at<const f32x4>(OP(3), i)), m = ld(at<const f32x4>(OP(4), i)), v = ld(at<const f32x4>(OP(5), i));
+    if (a.init_mv) {
+      dM = ld(at<const f32x4>(OP(1), i));
+      dV = ld(at<const f32x4>(OP(2), i));
+    }
+    for (int s = 0; s < a.K; ++s) {
+      f32x4 gn = g, mn = m, vn = v;
+      if (s + 1 < a.K) {
+        gn = ld(at<const f32x4>(OP(3 + 4 * (s + 1)), i));
+        mn = ld(at<const f32x4>(OP(4 + 4 * (s + 1)), i));
+        vn = ld(at<const f32x4>(OP(5 + 4 * (s + 1)), i));
+      }
+      f32x4 rg;
+      if (s == 0 && !a.init_mv) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const BwdOut o = bwd_elem<false>(dP[e], 0.0f, 0.0f, g[e], m[e], v[e], a.c[s]);
+          rg[e] = o.g;
+          dM[e] = o.m;
+          dV[e] = o.v;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const BwdOut o = bwd_elem<true>(dP[e], dM[e], dV[e], g[e], m[e], v[e], a.c[s]);
+          rg[e] = o.g;
+          dM[e] = o.m;
+          dV[e] = o.v;
+        }
+      }
+      st(at<f32x4>(OP(6 + 4 * s), i), rg);
+      g = gn;
+      m = mn;
+      v = vn;
+    }
+    st(at<f32x4>(OP(1), i), dM);
+    st(at<f32x4>(OP(2), i), dV);
+  } else {
+    const int64_t end = e0 + 4 < nel ? e0 + 4 : nel;
+    for (int64_t i = e0; i < end; ++i) {
+      const float dP = *at<const float>(OP(0), i);
+      float dM = 0.0f, dV = 0.0f;
+      if (a.init_mv) {
+        dM = *at<const float>(OP(1), i);
+        dV = *at<const float>(OP(2), i);
+      }
+      for (int s = 0; s < a.K; ++s) {
+        const float g = *at<const float>(OP(3 + 4 * s), i), m = *at<const float>(OP(4 + 4 * s), i),
+                    v = *at<const float>(OP(5 + 4 * s), i);
+        const BwdOut o = (s == 0 && !a.init_mv) ? bwd_elem<false>(dP, 0.0f, 0.0f, g, m, v, a.c[s])
+                                                : bwd_elem<true>(dP, dM, dV, g, m, v, a.c[s]);
+        *at<float>(OP(6 + 4 * s), i) = o.g;
+        dM = o.m;
+        dV = o.v;
+      }
+      *at<float>(OP(1), i) = dM;
+      *at<float>(OP(2), i) = dV;
+    }
+  }
+#undef OP
+}
+
 int check_table(const char* who, const diffopt_segtable* t) {
   if (!t) return fail(DIFFOPT_EINVAL, "%s: table is NULL", who);
   if (t->elem_bytes != 4) return fail(DIFFOPT_EINVAL, "%s: the table must describe fp32 leaves (elem_bytes 4)", who);
@@ -325,11 +519,23 @@ extern "C" int diffopt_adam_unrolled_fwd_tree(const diffopt_segtable* table, int
     if (k < K && !grads[k]) return fail(DIFFOPT_EINVAL, "%s: null grads entry %lld", who, (long long)k);
   }
   hipStream_t st = as_stream(stream);
-  for (int64_t k = 1; k <= K; ++k) {
-    make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &c);
-    const LeafArrays<7> arr{{k == 1 ? p0 : pK, grads[k - 1], mu_traj[k - 1], nu_traj[k - 1], pK, mu_traj[k],
-                             nu_traj[k]}};
-    rc = launch_fwd_tree(table, arr, c, st);
+  for (int64_t k0 = 0; k0 < K; k0 += kTK) {  // one fused launch per kTK steps
+    TFwdArgs a{};
+    a.K = (int32_t)(K - k0 < kTK ? K - k0 : kTK);
+    a.a[0] = (k0 == 0) ? p0 : pK;
+    a.a[1] = mu_traj[k0];
+    a.a[2] = nu_traj[k0];
+    a.a[3] = pK;
+    for (int s = 0; s < a.K; ++s) {
+      a.a[4 + 3 * s] = grads[k0 + s];
+      a.a[5 + 3 * s] = mu_traj[k0 + s + 1];
+      a.a[6 + 3 * s] = nu_traj[k0 + s + 1];
+      make_coef(who, count0 + k0 + s, lr, b1, b2, eps, eps_root, &a.c[s]);
+    }
+    const size_t lds = sizeof(uint64_t) * kWindowMax * (4 + 3 * a.K);
+    hipLaunchKernelGGL(adam_unrolled_fwd_tree_kernel, dim3((unsigned)table->ntiles), dim3(kUTB), lds, st,
+                       table->d_seg, table->d_tile_first, table->ngroups, table->dense_orig, a);
+    rc = launch_status(who);
     if (rc) return rc;
   }
   return DIFFOPT_OK;
@@ -359,12 +565,25 @@ extern "C" int diffopt_adam_unrolled_bwd_tree(const diffopt_segtable* table, int
       return fail(DIFFOPT_EINVAL, "%s: null entry %lld in a pointer array", who, (long long)k);
   }
   hipStream_t st = as_stream(stream);
-  for (int64_t k = K; k >= 1; --k) {
-    make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &c);
-    const bool first = (k == K);  // zero cotangents of mu_K, nu_K
-    const LeafArrays<9> arr{{dpK, first ? nullptr : dmu0, first ? nullptr : dnu0, grads[k - 1], mu_traj[k - 1],
-                             nu_traj[k - 1], dgrads[k - 1], dmu0, dnu0}};
-    rc = launch_bwd_tree(table, arr, c, st);
+  for (int64_t khi = K; khi >= 1; khi -= kTK) {  // one fused launch per kTK steps, last steps first
+    TBwdArgs a{};
+    a.K = (int32_t)(khi < kTK ? khi : kTK);
+    a.init_mv = khi != K;  // the first launch starts from zero cotangents of mu_K, nu_K
+    a.a[0] = dpK;
+    a.a[1] = dmu0;
+    a.a[2] = dnu0;
+    for (int s = 0; s < a.K; ++s) {
+      const int64_t k = khi - s;  // unrolled step (1-based) run as the launch's step s
+      a.a[3 + 4 * s] = grads[k - 1];
+      a.a[4 + 4 * s] = mu_traj[k - 1];
+      a.a[5 + 4 * s] = nu_traj[k - 1];
+      a.a[6 + 4 * s] = dgrads[k - 1];
+      make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &a.c[s]);
+    }
+    const size_t lds = sizeof(uint64_t) * kWindowMax * (3 + 4 * a.K);
+    hipLaunchKernelGGL(adam_unrolled_bwd_tree_kernel, dim3((unsigned)table->ntiles), dim3(kUTB), lds, st,
+                       table->d_seg, table->d_tile_first, table->ngroups, table->dense_orig, a);
+    rc = launch_status(who);
     if (rc) return rc;
   }
   return DIFFOPT_OK;
