@@ -330,7 +330,7 @@ int diffopt_rmsprop_bwd(const float* dparams_out, const float* dnu_out,
  *   noise       [num_samples][n], row-major (row i is z_i)
  *   out         [num_samples][n], row i = theta + sigma z_i; with antithetic != 0
  *               [2 num_samples][n], rows num_samples + i = theta - sigma z_i
- * num_samples <= 524,280.  n % 4 == 0 with 16-byte aligned pointers takes
+ * num_samples <= 65,535 x 8.  n % 4 == 0 with 16-byte aligned pointers takes
  * 128-bit accesses; anything else an element path with the same result.    */
 int diffopt_es_perturb(const float* params, const float* noise,
                        int64_t num_samples, int64_t n, double sigma,

@@ -12,31 +12,56 @@
 
 #include "adam_math.hpp"
 
+#ifndef DIFFOPT_ES_PERTURB_ROWS
+#define DIFFOPT_ES_PERTURB_ROWS 8
+#endif
+
 namespace diffopt {
 namespace {
 
 constexpr int kEB = 256;   // threads per workgroup
-constexpr int kRows = 8;   // noise rows per workgroup in perturb (theta reuse)
+constexpr int kRows = DIFFOPT_ES_PERTURB_ROWS;  // noise rows per workgroup in perturb
 constexpr int kUnroll = 8; // rows in flight per lane in estimate
 
-// Grid: x over 16-byte vectors of theta, y over groups of kRows samples.
+// Grid: x over 16-byte vectors of theta, y over groups of kRows samples.  The
+// dispatcher walks x fastest, so the chip works through the rows a group at a
+// time (few DRAM pages open at once); theta is re-read per group, mostly from
+// the Infinity Cache.  A lane issues all of its group's row loads first.
 __global__ __launch_bounds__(kEB) void es_perturb_vec(const float* theta, const float* noise, int64_t N,
                                                        int64_t nv, float sigma, int antithetic, float* out) {
   const int64_t v = (int64_t)blockIdx.x * kEB + threadIdx.x;
   if (v >= nv) return;
-  const f32x4 t = ld(reinterpret_cast<const f32x4*>(theta) + v);
   const int64_t i0 = (int64_t)blockIdx.y * kRows;
-  const int64_t i1 = i0 + kRows < N ? i0 + kRows : N;
-  for (int64_t i = i0; i < i1; ++i) {
-    const f32x4 z = ld(reinterpret_cast<const f32x4*>(noise) + i * nv + v);
-    f32x4 a, b;
+  const f32x4 t = ld(reinterpret_cast<const f32x4*>(theta) + v);
+  const f32x4* z = reinterpret_cast<const f32x4*>(noise) + v;
+  f32x4* o = reinterpret_cast<f32x4*>(out) + v;
+  if (i0 + kRows <= N) {
+    f32x4 r[kRows];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      a[e] = fmaf(sigma, z[e], t[e]);
-      b[e] = fmaf(-sigma, z[e], t[e]);
+    for (int u = 0; u < kRows; ++u) r[u] = ld(z + (i0 + u) * nv);
+#pragma unroll
+    for (int u = 0; u < kRows; ++u) {
+      f32x4 a, b;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a[e] = fmaf(sigma, r[u][e], t[e]);
+        b[e] = fmaf(-sigma, r[u][e], t[e]);
+      }
+      st(o + (i0 + u) * nv, a);
+      if (antithetic) st(o + (N + i0 + u) * nv, b);
     }
-    st(reinterpret_cast<f32x4*>(out) + i * nv + v, a);
-    if (antithetic) st(reinterpret_cast<f32x4*>(out) + (N + i) * nv + v, b);
+  } else {
+    for (int64_t i = i0; i < N; ++i) {
+      const f32x4 r = ld(z + i * nv);
+      f32x4 a, b;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a[e] = fmaf(sigma, r[e], t[e]);
+        b[e] = fmaf(-sigma, r[e], t[e]);
+      }
+      st(o + i * nv, a);
+      if (antithetic) st(o + (N + i) * nv, b);
+    }
   }
 }
 
