@@ -45,6 +45,9 @@ UNROLL_CHUNK = 16   # steps per launch of the fused K-step driver
 TREE_UNROLL_CHUNK = 8  # the same for its leaf-direct form
 
 
+REMAT_SPAN = 8      # longest run of steps whose moments the backward recomputes
+
+
 def b_unrolled_fwd(K):
     """K fused forward steps: p0, mu0, nu0 and K gradients in; K (mu, nu) and p_K out."""
     return 16 + 12 * K
@@ -55,6 +58,53 @@ def b_unrolled_bwd(K):
     return 12 + 16 * K
 
 
+def stored_states(K, trajectory):
+    """Indices 1..K of the moment states the forward stores: all of them, or
+    (recompute) only the final one and every REMAT_SPAN-th."""
+    if trajectory == "stored":
+        return set(range(1, K + 1))
+    return set(range(REMAT_SPAN, K, REMAT_SPAN)) | {K}
+
+
+def fwd_plan(K, stored, chunk):
+    """(launches, interface bytes per element) of the fused K-step forward:
+    per launch p, mu, nu in and p out, one gradient per step, and mu, nu out
+    for every stored state (a launch boundary on an unstored state passes the
+    running moments through the final-state buffers: one more pair out)."""
+    launches, b = 0, 0
+    for k0 in range(0, K, chunk):
+        k1 = min(K, k0 + chunk)
+        launches += 1
+        outs = sum(1 for k in range(k0 + 1, k1 + 1) if k in stored or k == k1)
+        b += 16 + 4 * (k1 - k0) + 8 * outs
+    return launches, b
+
+
+def bwd_plan(K, stored, chunk):
+    """(launches, interface bytes per element) of the fused K-step VJP, as the
+    driver plans it, last steps first: a run of steps whose input states are
+    stored (at most `chunk`) reads g, mu, nu per step; a run j+1..khi whose
+    states j+1..khi-1 are not stored reads mu_j, nu_j once and recomputes the
+    rest.  Every launch reads dP, writes dg per step and dmu, dnu, and reads
+    the running dmu, dnu unless it holds step K."""
+    have = set(stored) | {0}
+    launches, b, khi = 0, 0, K
+    while khi >= 1:
+        launches += 1
+        b += 4 + 8 + (8 if khi != K else 0)
+        if khi - 1 in have:
+            run = 0
+            while run < chunk and khi - run >= 1 and (khi - run - 1) in have:
+                run += 1
+            b += 16 * run
+            khi -= run
+        else:
+            j = max(x for x in have if x < khi)
+            b += 8 + 8 * (khi - j)
+            khi = j
+    return launches, b
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -63,6 +113,9 @@ def parse():
     ap.add_argument("--workload", default="many_small",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
                              "many_small_treemap", "sgd_flat", "rmsprop_flat", "es_resnet18"])
+    ap.add_argument("--trajectory", choices=["stored", "recompute"], default="recompute",
+                    help="K-step driver: store every moment state for the backward, or store only the final one "
+                         "(and every %d-th) and let the backward recompute the rest in registers" % REMAT_SPAN)
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time replays (no per-phase split)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -115,7 +168,7 @@ def traffic_from_profile(kernel, workload):
 # --------------------------------------------------------------------- setup
 
 
-def setup_tree(torch, P, w):
+def setup_tree(torch, P, w, trajectory):
     from workloads import HYPER, torch_normal
     K, n, numel = w.K, w.n, w.numels
     dev = "cuda"
@@ -139,13 +192,14 @@ def setup_tree(torch, P, w):
     dg_trees = [[torch.empty_like(x) for x in p_tree] for _ in range(K)]
     z = lambda: torch.zeros(n, dtype=torch.float32, device=dev)  # noqa: E731
     e = lambda: torch.empty(n, dtype=torch.float32, device=dev)  # noqa: E731
+    stored = stored_states(K, trajectory)
     S = dict(
         K=K, n=n, table=table, hyper=dict(HYPER, eps_root=w.eps_root), count0=w.count0,
         p_ptrs=ptrs(p_tree), g_ptrs=[ptrs(t) for t in g_trees],
         pK_ptrs=ptrs(pK_tree), dg_ptrs=[ptrs(t) for t in dg_trees],
-        p0=e(), g=[e() for _ in range(K)], mu=[z()] + [e() for _ in range(K)],
-        nu=[z()] + [e() for _ in range(K)], pK=e(), cot=torch_normal(n, 1.0, 120, dev),
-        dg=[e() for _ in range(K)], dm0=e(), dv0=e(),
+        p0=e(), g=[e() for _ in range(K)], mu=[z()] + [e() if k in stored else None for k in range(1, K + 1)],
+        nu=[z()] + [e() if k in stored else None for k in range(1, K + 1)], pK=e(),
+        cot=torch_normal(n, 1.0, 120, dev), dg=[e() for _ in range(K)], dm0=e(), dv0=e(), stored=stored,
         keep=(p_tree, g_trees, pK_tree, dg_trees),
     )
     return S
@@ -178,10 +232,12 @@ def step_tree(P, S, ev=None):
 def phases_tree(S):
     """(name, kernel, launches per step, algorithmic bytes per step) per phase."""
     K, n = S["K"], S["n"]
+    fl, fb = fwd_plan(K, S["stored"], UNROLL_CHUNK)
+    bl, bb = bwd_plan(K, S["stored"], UNROLL_CHUNK)
     return [
         ("flatten", "tree_flatten", K + 1, (K + 1) * B_COPY * n),
-        ("adam_fwd", "adam_unrolled_fwd", -(-K // UNROLL_CHUNK), b_unrolled_fwd(K) * n),
-        ("adam_bwd", "adam_unrolled_bwd", -(-K // UNROLL_CHUNK), b_unrolled_bwd(K) * n),
+        ("adam_fwd", "adam_unrolled_fwd", fl, fb * n),
+        ("adam_bwd", "adam_unrolled_bwd", bl, bb * n),
         ("unflatten", "tree_unflatten", K + 1, (K + 1) * B_COPY * n),
     ]
 
@@ -457,7 +513,7 @@ def main():
     elif a.workload == "many_small_treemap":
         S, step, phases = setup_treemap(torch, P, w), step_treemap, phases_treemap
     else:
-        S, step, phases = setup_tree(torch, P, w), step_tree, phases_tree
+        S, step, phases = setup_tree(torch, P, w, a.trajectory), step_tree, phases_tree
     ph = phases(S)
     nph = len(ph)
     torch.cuda.synchronize()

@@ -46,6 +46,10 @@ extern "C" {
 #define DIFFOPT_ENOMEM (-2) /* host or device allocation failed             */
 #define DIFFOPT_EHIP (-3)   /* a HIP runtime call or kernel launch failed   */
 
+/* Longest run of unrolled steps whose moment trajectory the K-step backward
+ * recomputes from one stored state (see diffopt_adam_unrolled_bwd).        */
+#define DIFFOPT_REMAT_SPAN 8
+
 /* Message describing the last nonzero return on this thread ("" if none).
  * The pointer stays valid until the next diffopt call on the same thread. */
 const char* diffopt_last_error(void);
@@ -162,17 +166,25 @@ int diffopt_adam_bwd(const float* dupdate, const float* dmu, const float* dnu,
  *   p0          input [n] (not modified unless pK == p0)
  *   grads       HOST array [K] of device pointers, grads[k-1] = g_k
  *   mu_traj     HOST array [K+1] of device pointers: mu_traj[0] = mu0 is
- *               read, mu_traj[k] receives mu_k (the trajectory the backward
- *               needs); all K+1 buffers distinct
- *   nu_traj     the same for nu
+ *               read, mu_traj[k] receives mu_k.  mu_traj[0] and mu_traj[K]
+ *               (the final state) are required; an intermediate entry
+ *               (0 < k < K) may be NULL, and that state is then not stored
+ *               (the backward recomputes it, see below).  Non-NULL entries
+ *               are distinct buffers
+ *   nu_traj     the same for nu; nu_traj[k] is NULL exactly when mu_traj[k]
+ *               is
  *   pK          output [n] (may equal p0)
- * grads, mu_traj[1..K], nu_traj[1..K] and pK must not overlap one another or
- * p0, mu_traj[0], nu_traj[0] (pK == p0 excepted).
+ * grads, the stored mu_traj[1..K], nu_traj[1..K] and pK must not overlap one
+ * another or p0, mu_traj[0], nu_traj[0] (pK == p0 excepted).
  * The K steps run fused, one kernel per 16 steps: each element's running
- * params stay in registers between steps, so K steps move 16 + 12K bytes per
- * element.  The result equals K calls of diffopt_adam_fwd bit for bit.  With
- * any pointer not 16-byte aligned it enqueues K single-step kernels instead
- * (same result).  No host synchronisation.                                  */
+ * params and moments stay in registers between steps, so K steps move
+ * 16 + 4K + 8 S bytes per element for S stored states (16 + 12K with the
+ * whole trajectory, 24 + 4K with the final state only).  When a 16-step
+ * launch boundary falls on an unstored state, the running moments pass to the
+ * next launch through mu_traj[K], nu_traj[K].  Every stored state and pK
+ * equal K calls of diffopt_adam_fwd bit for bit.  Pointers that are not
+ * 16-byte aligned take a one-element-per-lane kernel with the same result.
+ * No host synchronisation.                                                  */
 int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0,
                               const float* const* grads,
                               float* const* mu_traj, float* const* nu_traj,
@@ -188,17 +200,27 @@ int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0,
  *   dpK         input [n]; the cotangent of p0 equals dpK (identity), so it
  *               is not copied
  *   grads, mu_traj, nu_traj   as given to / written by the forward (HOST
- *               arrays of device pointers; mu_traj[K], nu_traj[K] unused)
+ *               arrays of device pointers; mu_traj[K], nu_traj[K] unused).
+ *               A NULL intermediate entry k is recomputed from the latest
+ *               stored state j < k and g_{j+1..k} with the forward's own
+ *               recurrences, so the result is the same bit for bit; at most
+ *               DIFFOPT_REMAT_SPAN - 1 consecutive entries may be NULL
+ *               (EINVAL otherwise, before anything is enqueued)
  *   dgrads      HOST array [K] of device pointers: dgrads[k-1] receives the
  *               cotangent of g_k
  *   dmu0, dnu0  outputs [n]: cotangents of mu0, nu0 (also the running dM,
- *               dV between launches when K > 16)
+ *               dV between launches)
  * Outputs must not overlap the inputs or one another.
- * The K steps run fused, last step first, one kernel per 16 steps: each
- * element's dM, dV stay in registers, so K steps move 12 + 16K bytes per
- * element.  The result equals K calls of diffopt_adam_bwd (the first with
- * zero dM, dV) bit for bit.  With any pointer not 16-byte aligned it
- * enqueues those K single-step kernels instead.                             */
+ * The K steps run fused, last step first, with each element's dM, dV in
+ * registers: a run of steps whose input states are stored takes one launch
+ * per 16 steps and reads each state back (12 + 16K bytes per element for
+ * the whole trajectory); a run of C <= DIFFOPT_REMAT_SPAN steps after one
+ * stored state takes one launch that reads that state and the C gradients
+ * once, recomputes the run's states in registers, then runs its VJP steps
+ * (20 + 8K bytes per element for K <= DIFFOPT_REMAT_SPAN with nothing
+ * stored).  The result equals K calls of diffopt_adam_bwd (the first with
+ * zero dM, dV) on the full trajectory bit for bit.  Pointers that are not
+ * 16-byte aligned take one-element-per-lane kernels with the same result. */
 int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
                               const float* const* grads,
                               const float* const* mu_traj,

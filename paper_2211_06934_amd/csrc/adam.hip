@@ -35,6 +35,9 @@
 #ifndef DIFFOPT_UBWD_BLOCK
 #define DIFFOPT_UBWD_BLOCK 1024  // threads per workgroup, fused K-step VJP
 #endif
+#ifndef DIFFOPT_URBWD_BLOCK
+#define DIFFOPT_URBWD_BLOCK 256  // threads per workgroup, fused VJP recomputing the moments
+#endif
 
 namespace diffopt {
 
@@ -73,6 +76,16 @@ int make_coef(const char* who, int64_t count, double lr, double b1, double b2, d
 }
 
 namespace {
+
+inline bool aligned16(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline bool aligned4(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+// One workgroup per tile; the kernels' grid-stride loop covers the (never
+// reached in practice) case of more tiles than a grid dimension holds.
+int64_t grid_for(int64_t tiles) {
+  if (tiles < 1) return 1;
+  return tiles < 0x7fffffff ? tiles : 0x7fffffff;
+}
 
 // ---- kernels -----------------------------------------------------------------
 // Vector kernels: tile t covers 16-byte vectors [t*B*U, (t+1)*B*U) for B
@@ -267,7 +280,7 @@ struct UFwdArgs {
   const float* v0;
   float* pK;  // params after the last step
   const float* g[kUK];
-  float* m[kUK];  // mu, nu after step s
+  float* m[kUK];  // mu, nu after step s; NULL: not stored (never for the last step)
   float* v[kUK];
   AdamCoef c[kUK];
   int64_t n;
@@ -306,8 +319,10 @@ __device__ __forceinline__ void ufwd_vector(int64_t i, const UFwdArgs& a) {
       M[e] = o.m;
       V[e] = o.v;
     }
-    st(v4(a.m[s]) + i, M);
-    st(v4(a.v[s]) + i, V);
+    if (a.m[s]) {  // uniform: the same for every lane
+      st(v4(a.m[s]) + i, M);
+      st(v4(a.v[s]) + i, V);
+    }
     G = Gn;
   }
   st(v4(a.pK) + i, P);
@@ -320,8 +335,10 @@ __device__ __forceinline__ void ufwd_element(int64_t e, const UFwdArgs& a) {
     P = o.p;
     M = o.m;
     V = o.v;
-    a.m[s][e] = M;
-    a.v[s][e] = V;
+    if (a.m[s]) {
+      a.m[s][e] = M;
+      a.v[s][e] = V;
+    }
   }
   a.pK[e] = P;
 }
@@ -340,6 +357,12 @@ __global__ __launch_bounds__(kUFB) void adam_unrolled_fwd_vec(UFwdArgs a) {
     const int64_t e = (nv << 2) + threadIdx.x;
     if (e < a.n) ufwd_element(e, a);
   }
+}
+
+// Any alignment: one element per thread (pointers only 4-byte aligned).
+__global__ __launch_bounds__(kUFB) void adam_unrolled_fwd_elem(UFwdArgs a) {
+  for (int64_t e = (int64_t)blockIdx.x * kUFB + threadIdx.x; e < a.n; e += (int64_t)gridDim.x * kUFB)
+    ufwd_element(e, a);
 }
 
 template <bool HAS_MV>
@@ -430,17 +453,143 @@ __global__ __launch_bounds__(kUBB) void adam_unrolled_bwd_vec(UBwdArgs a) {
   }
 }
 
-// ---- host launchers ------------------------------------------------------------
-
-inline bool aligned16(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-inline bool aligned4(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
-
-// One workgroup per tile; the kernels' grid-stride loop covers the (never
-// reached in practice) case of more tiles than a grid dimension holds.
-int64_t grid_for(int64_t tiles) {
-  if (tiles < 1) return 1;
-  return tiles < 0x7fffffff ? tiles : 0x7fffffff;
+__global__ __launch_bounds__(kUBB) void adam_unrolled_bwd_elem(UBwdArgs a) {
+  for (int64_t e = (int64_t)blockIdx.x * kUBB + threadIdx.x; e < a.n; e += (int64_t)gridDim.x * kUBB)
+    ubwd_element(e, a);
 }
+
+// ---- fused K-step VJP over a run of steps whose moments were not stored -------------
+// For a run of C steps j+1..j+C of which only the state (mu_j, nu_j) before
+// the first was stored, the lane reads that state and the C gradients once,
+// recomputes mu_j+1..mu_j+C-1 (and nu) with the forward's own recurrences
+// into registers, then runs the C VJP steps last step first.  Bytes per
+// element: 12 + 8C (dP, mu_j, nu_j, C g in; C dg out; plus the running dM,
+// dV: 8 in unless this run holds the last unrolled step, 8 out), against
+// 12 + 16C when every state is read back.  Registers hold 3C vectors, so a
+// run is at most kRS steps: the caller stores at least every kRS-th state.
+constexpr int kRS = DIFFOPT_REMAT_SPAN;
+constexpr int kURB = DIFFOPT_URBWD_BLOCK;
+
+// Step s of a run is unrolled step j+1+s (ascending); the VJP walks s = C-1..0.
+struct URBwdArgs {
+  const float* dP;
+  float* dm;  // running dM, dV: read first if init_mv, written at the end
+  float* dv;
+  const float* m0;  // the stored state (mu_j, nu_j) before the run's first step
+  const float* v0;
+  const float* g[kRS];
+  float* dg[kRS];
+  AdamCoef c[kRS];
+  int64_t n;
+  int32_t init_mv;  // 0: the run holds the last unrolled step (zero dM, dV before it)
+};
+
+template <int C>
+__device__ __forceinline__ void urbwd_vector(int64_t i, const URBwdArgs& a) {
+  const f32x4 dP = ld(cv4(a.dP) + i);
+  f32x4 G[C], M[C], V[C];  // M[s], V[s]: the moments step s consumed
+  M[0] = ld(cv4(a.m0) + i);
+  V[0] = ld(cv4(a.v0) + i);
+#pragma unroll
+  for (int s = 0; s < C; ++s) G[s] = ld(cv4(a.g[s]) + i);
+  f32x4 dM = {0.0f, 0.0f, 0.0f, 0.0f}, dV = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (a.init_mv) {
+    dM = ld(cv4(a.dm) + i);
+    dV = ld(cv4(a.dv) + i);
+  }
+#pragma unroll
+  for (int s = 0; s + 1 < C; ++s) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      M[s + 1][e] = moment1(G[s][e], M[s][e], a.c[s]);
+      V[s + 1][e] = moment2(G[s][e], V[s][e], a.c[s]);
+    }
+  }
+  if (a.init_mv) ubwd_step<true>(dP, dM, dV, G[C - 1], M[C - 1], V[C - 1], a.c[C - 1], v4(a.dg[C - 1]) + i);
+  else ubwd_step<false>(dP, dM, dV, G[C - 1], M[C - 1], V[C - 1], a.c[C - 1], v4(a.dg[C - 1]) + i);
+#pragma unroll
+  for (int s = C - 2; s >= 0; --s) ubwd_step<true>(dP, dM, dV, G[s], M[s], V[s], a.c[s], v4(a.dg[s]) + i);
+  st(v4(a.dm) + i, dM);
+  st(v4(a.dv) + i, dV);
+}
+
+template <int C>
+__device__ __forceinline__ void urbwd_element(int64_t e, const URBwdArgs& a) {
+  const float dP = a.dP[e];
+  float G[C], M[C], V[C];
+  M[0] = a.m0[e];
+  V[0] = a.v0[e];
+#pragma unroll
+  for (int s = 0; s < C; ++s) G[s] = a.g[s][e];
+#pragma unroll
+  for (int s = 0; s + 1 < C; ++s) {
+    M[s + 1] = moment1(G[s], M[s], a.c[s]);
+    V[s + 1] = moment2(G[s], V[s], a.c[s]);
+  }
+  float dM = 0.0f, dV = 0.0f;
+  BwdOut o;
+  if (a.init_mv) o = bwd_elem<true>(dP, a.dm[e], a.dv[e], G[C - 1], M[C - 1], V[C - 1], a.c[C - 1]);
+  else o = bwd_elem<false>(dP, 0.0f, 0.0f, G[C - 1], M[C - 1], V[C - 1], a.c[C - 1]);
+  a.dg[C - 1][e] = o.g;
+  dM = o.m;
+  dV = o.v;
+#pragma unroll
+  for (int s = C - 2; s >= 0; --s) {
+    o = bwd_elem<true>(dP, dM, dV, G[s], M[s], V[s], a.c[s]);
+    a.dg[s][e] = o.g;
+    dM = o.m;
+    dV = o.v;
+  }
+  a.dm[e] = dM;
+  a.dv[e] = dV;
+}
+
+template <int C>
+__global__ __launch_bounds__(kURB) void adam_unrolled_bwd_remat_vec(URBwdArgs a) {
+  const int64_t nv = a.n >> 2;
+  const int64_t ntiles = (nv + kURB - 1) / kURB;
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t i = t * kURB + threadIdx.x;
+    if (i < nv) urbwd_vector<C>(i, a);
+  }
+  if (blockIdx.x == gridDim.x - 1) {
+    const int64_t e = (nv << 2) + threadIdx.x;
+    if (e < a.n) urbwd_element<C>(e, a);
+  }
+}
+
+template <int C>
+__global__ __launch_bounds__(kURB) void adam_unrolled_bwd_remat_elem(URBwdArgs a) {
+  for (int64_t e = (int64_t)blockIdx.x * kURB + threadIdx.x; e < a.n; e += (int64_t)gridDim.x * kURB)
+    urbwd_element<C>(e, a);
+}
+
+template <int C>
+void launch_urbwd(bool vec, const URBwdArgs& a, hipStream_t st) {
+  if (vec)
+    hipLaunchKernelGGL((adam_unrolled_bwd_remat_vec<C>), dim3((unsigned)grid_for(((a.n >> 2) + kURB - 1) / kURB)),
+                       dim3(kURB), 0, st, a);
+  else
+    hipLaunchKernelGGL((adam_unrolled_bwd_remat_elem<C>), dim3((unsigned)grid_for((a.n + kURB - 1) / kURB)),
+                       dim3(kURB), 0, st, a);
+}
+
+// Run length C is a template argument so the trajectory stays in registers.
+void launch_urbwd_c(int C, bool vec, const URBwdArgs& a, hipStream_t st) {
+  switch (C) {
+    case 1: launch_urbwd<1>(vec, a, st); break;
+    case 2: launch_urbwd<2>(vec, a, st); break;
+    case 3: launch_urbwd<3>(vec, a, st); break;
+    case 4: launch_urbwd<4>(vec, a, st); break;
+    case 5: launch_urbwd<5>(vec, a, st); break;
+    case 6: launch_urbwd<6>(vec, a, st); break;
+    case 7: launch_urbwd<7>(vec, a, st); break;
+    default: launch_urbwd<8>(vec, a, st); break;
+  }
+}
+static_assert(kRS == 8, "launch_urbwd_c instantiates run lengths 1..8");
+
+// ---- host launchers ------------------------------------------------------------
 
 int launch_fwd(const float* p, const float* g, const float* m, const float* v, int64_t n, const AdamCoef& c,
                float* po, float* mo, float* vo, float* uo, hipStream_t st) {
@@ -544,6 +693,35 @@ extern "C" int diffopt_adam_bwd(const float* dupdate, const float* dmu, const fl
   return launch_bwd(dupdate, dmu, dnu, grad, mu, nu, n, c, dparams, dgrad, dmu_in, dnu_in, as_stream(stream));
 }
 
+namespace diffopt {
+namespace {
+
+// Stored-state bookkeeping shared by both drivers: entry k (1..K-1) of a
+// trajectory may be NULL (not stored), mu and nu together.  The backward
+// (bound_runs) recomputes a NULL state from the latest stored one before it,
+// in registers, so at most kRS - 1 consecutive entries may be NULL.
+int check_trajectory(const char* who, int64_t K, const float* const* mu_traj, const float* const* nu_traj,
+                     bool need_last, bool bound_runs) {
+  if (!mu_traj[0] || !nu_traj[0]) return fail(DIFFOPT_EINVAL, "%s: null initial state mu_traj[0] / nu_traj[0]", who);
+  if (need_last && (!mu_traj[K] || !nu_traj[K]))
+    return fail(DIFFOPT_EINVAL, "%s: null final state mu_traj[K] / nu_traj[K]", who);
+  int64_t last = 0;  // latest stored state
+  for (int64_t k = 1; k < K; ++k) {
+    if ((mu_traj[k] == nullptr) != (nu_traj[k] == nullptr))
+      return fail(DIFFOPT_EINVAL, "%s: trajectory entry %lld: mu and nu must both be stored or both be NULL", who,
+                  (long long)k);
+    if (mu_traj[k]) last = k;
+    else if (bound_runs && k + 1 - last > kRS)
+      return fail(DIFFOPT_EINVAL,
+                  "%s: trajectory entries %lld..%lld are all NULL; at least every %d-th state must be stored", who,
+                  (long long)(last + 1), (long long)k, kRS);
+  }
+  return DIFFOPT_OK;
+}
+
+}  // namespace
+}  // namespace diffopt
+
 extern "C" int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0, const float* const* grads,
                                          float* const* mu_traj, float* const* nu_traj, float* pK, int64_t count0,
                                          double lr, double b1, double b2, double eps, double eps_root,
@@ -560,45 +738,47 @@ extern "C" int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0, 
   }
   if (n == 0) return DIFFOPT_OK;
   if (!p0 || !pK) return fail(DIFFOPT_EINVAL, "%s: null p0 or pK", who);
-  for (int64_t k = 0; k <= K; ++k) {
-    if (!mu_traj[k] || !nu_traj[k]) return fail(DIFFOPT_EINVAL, "%s: null trajectory entry %lld", who, (long long)k);
-    if (k < K && !grads[k]) return fail(DIFFOPT_EINVAL, "%s: null grads entry %lld", who, (long long)k);
-  }
+  for (int64_t k = 0; k < K; ++k)
+    if (!grads[k]) return fail(DIFFOPT_EINVAL, "%s: null grads entry %lld", who, (long long)k);
+  int rc = check_trajectory(who, K, mu_traj, nu_traj, true, false);
+  if (rc) return rc;
   hipStream_t st = as_stream(stream);
   bool vec = aligned16(p0) && aligned16(pK);
   for (int64_t k = 0; k <= K; ++k) {
     vec = vec && aligned16(mu_traj[k]) && aligned16(nu_traj[k]);
     if (k < K) vec = vec && aligned16(grads[k]);
   }
-  if (vec) {  // fused: one launch per kUK steps
-    for (int64_t k0 = 0; k0 < K; k0 += kUK) {
-      UFwdArgs a;
-      a.K = (int32_t)(K - k0 < kUK ? K - k0 : kUK);
-      a.n = n;
-      a.p = (k0 == 0) ? p0 : pK;
-      a.m0 = mu_traj[k0];
-      a.v0 = nu_traj[k0];
-      a.pK = pK;
-      for (int s = 0; s < kUK; ++s) {
-        const bool on = s < a.K;
-        a.g[s] = on ? grads[k0 + s] : nullptr;
-        a.m[s] = on ? mu_traj[k0 + s + 1] : nullptr;
-        a.v[s] = on ? nu_traj[k0 + s + 1] : nullptr;
-        if (on) make_coef(who, count0 + k0 + s, lr, b1, b2, eps, eps_root, &a.c[s]);
-        else a.c[s] = AdamCoef{};
-      }
-      const int64_t blocks = grid_for(((n >> 2) + kUFB - 1) / kUFB);
-      hipLaunchKernelGGL(adam_unrolled_fwd_vec, dim3((unsigned)blocks), dim3(kUFB), 0, st, a);
-      int rc = launch_status(who);
-      if (rc) return rc;
+  for (int64_t k0 = 0; k0 < K; k0 += kUK) {  // one fused launch per kUK steps
+    UFwdArgs a;
+    a.K = (int32_t)(K - k0 < kUK ? K - k0 : kUK);
+    a.n = n;
+    // Between launches the running params pass through pK.  The running
+    // moments pass through the state stored at the boundary, or, when that
+    // entry is NULL, through the final-state buffers mu_traj[K], nu_traj[K]
+    // (each lane reads its elements there before writing them).
+    a.p = (k0 == 0) ? p0 : pK;
+    a.m0 = mu_traj[k0] ? mu_traj[k0] : mu_traj[K];
+    a.v0 = nu_traj[k0] ? nu_traj[k0] : nu_traj[K];
+    a.pK = pK;
+    for (int s = 0; s < kUK; ++s) {
+      const bool on = s < a.K;
+      a.g[s] = on ? grads[k0 + s] : nullptr;
+      a.m[s] = on ? mu_traj[k0 + s + 1] : nullptr;
+      a.v[s] = on ? nu_traj[k0 + s + 1] : nullptr;
+      if (on) make_coef(who, count0 + k0 + s, lr, b1, b2, eps, eps_root, &a.c[s]);
+      else a.c[s] = AdamCoef{};
     }
-    return DIFFOPT_OK;
-  }
-  for (int64_t k = 1; k <= K; ++k) {  // any pointer not 16-byte aligned: step by step
-    make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &c);
-    const float* src = (k == 1) ? p0 : pK;
-    int rc = launch_fwd(src, grads[k - 1], mu_traj[k - 1], nu_traj[k - 1], n, c, pK, mu_traj[k], nu_traj[k],
-                        nullptr, st);
+    if (!a.m[a.K - 1]) {  // boundary state not stored: carry it in the final-state buffers
+      a.m[a.K - 1] = mu_traj[K];
+      a.v[a.K - 1] = nu_traj[K];
+    }
+    if (vec)
+      hipLaunchKernelGGL(adam_unrolled_fwd_vec, dim3((unsigned)grid_for(((n >> 2) + kUFB - 1) / kUFB)), dim3(kUFB),
+                         0, st, a);
+    else  // some pointer is not 16-byte aligned: one element per lane, same arithmetic
+      hipLaunchKernelGGL(adam_unrolled_fwd_elem, dim3((unsigned)grid_for((n + kUFB - 1) / kUFB)), dim3(kUFB), 0, st,
+                         a);
+    rc = launch_status(who);
     if (rc) return rc;
   }
   return DIFFOPT_OK;
@@ -621,23 +801,30 @@ extern "C" int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
   if (n == 0) return DIFFOPT_OK;
   if (!dpK || !dmu0 || !dnu0) return fail(DIFFOPT_EINVAL, "%s: null dpK, dmu0 or dnu0", who);
   if (dmu0 == dnu0) return fail(DIFFOPT_EINVAL, "%s: dmu0 and dnu0 must be distinct", who);
-  for (int64_t k = 0; k < K; ++k) {
-    if (!grads[k] || !mu_traj[k] || !nu_traj[k] || !dgrads[k])
-      return fail(DIFFOPT_EINVAL, "%s: null entry %lld in a pointer array", who, (long long)k);
-  }
+  for (int64_t k = 0; k < K; ++k)
+    if (!grads[k] || !dgrads[k]) return fail(DIFFOPT_EINVAL, "%s: null entry %lld in grads or dgrads", who,
+                                             (long long)k);
+  int rc = check_trajectory(who, K, mu_traj, nu_traj, false, true);
+  if (rc) return rc;
   hipStream_t st = as_stream(stream);
   bool vec = aligned16(dpK) && aligned16(dmu0) && aligned16(dnu0);
   for (int64_t k = 0; k < K; ++k)
     vec = vec && aligned16(grads[k]) && aligned16(mu_traj[k]) && aligned16(nu_traj[k]) && aligned16(dgrads[k]);
-  if (vec) {  // fused: one launch per kUK steps, last steps first
-    for (int64_t khi = K; khi >= 1; khi -= kUK) {
+  // Last steps first.  Steps whose input state was stored run up to kUK per
+  // launch, reading it back; a run of steps j+1..khi whose states were not
+  // stored (only mu_j, nu_j) runs in one launch that recomputes them.
+  for (int64_t khi = K; khi >= 1;) {
+    const bool init_mv = khi != K;  // the first launch starts from zero cotangents of mu_K, nu_K
+    if (mu_traj[khi - 1]) {
       UBwdArgs a;
-      a.K = (int32_t)(khi < kUK ? khi : kUK);
+      int32_t run = 0;
+      while (run < kUK && khi - run >= 1 && mu_traj[khi - run - 1]) ++run;
+      a.K = run;
       a.n = n;
       a.dP = dpK;
       a.dm = dmu0;
       a.dv = dnu0;
-      a.init_mv = khi != K;  // the first launch starts from zero cotangents of mu_K, nu_K
+      a.init_mv = init_mv;
       for (int s = 0; s < kUK; ++s) {
         const bool on = s < a.K;
         const int64_t k = khi - s;  // unrolled step (1-based) run as the launch's step s
@@ -648,18 +835,36 @@ extern "C" int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
         if (on) make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &a.c[s]);
         else a.c[s] = AdamCoef{};
       }
-      const int64_t blocks = grid_for(((n >> 2) + kUBB - 1) / kUBB);
-      hipLaunchKernelGGL(adam_unrolled_bwd_vec, dim3((unsigned)blocks), dim3(kUBB), 0, st, a);
-      int rc = launch_status(who);
-      if (rc) return rc;
+      if (vec)
+        hipLaunchKernelGGL(adam_unrolled_bwd_vec, dim3((unsigned)grid_for(((n >> 2) + kUBB - 1) / kUBB)),
+                           dim3(kUBB), 0, st, a);
+      else
+        hipLaunchKernelGGL(adam_unrolled_bwd_elem, dim3((unsigned)grid_for((n + kUBB - 1) / kUBB)), dim3(kUBB), 0,
+                           st, a);
+      khi -= run;
+    } else {
+      int64_t j = khi - 1;
+      while (!mu_traj[j]) --j;  // mu_traj[0] is stored; check_trajectory bounds khi - j by kRS
+      URBwdArgs a;
+      const int C = (int)(khi - j);
+      a.n = n;
+      a.dP = dpK;
+      a.dm = dmu0;
+      a.dv = dnu0;
+      a.m0 = mu_traj[j];
+      a.v0 = nu_traj[j];
+      a.init_mv = init_mv;
+      for (int s = 0; s < kRS; ++s) {
+        const bool on = s < C;
+        a.g[s] = on ? grads[j + s] : nullptr;
+        a.dg[s] = on ? dgrads[j + s] : nullptr;
+        if (on) make_coef(who, count0 + j + s, lr, b1, b2, eps, eps_root, &a.c[s]);
+        else a.c[s] = AdamCoef{};
+      }
+      launch_urbwd_c(C, vec, a, st);
+      khi = j;
     }
-    return DIFFOPT_OK;
-  }
-  for (int64_t k = K; k >= 1; --k) {  // any pointer not 16-byte aligned: step by step
-    make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &c);
-    const bool first = (k == K);  // zero cotangents of mu_K, nu_K
-    int rc = launch_bwd(dpK, first ? nullptr : dmu0, first ? nullptr : dnu0, grads[k - 1], mu_traj[k - 1],
-                        nu_traj[k - 1], n, c, nullptr, dgrads[k - 1], dmu0, dnu0, st);
+    rc = launch_status(who);
     if (rc) return rc;
   }
   return DIFFOPT_OK;

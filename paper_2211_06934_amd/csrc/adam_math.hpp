@@ -60,10 +60,19 @@ struct FwdOut {
   float p, m, v, u;
 };
 
+// The two moment recurrences of one step, m' = b1 m + (1-b1) g and
+// v' = b2 v + (1-b2) g^2.  Every kernel that forms m', v' (the step, its VJP,
+// the trajectory recomputation) goes through this one expression, so they all
+// agree bit for bit.
+__device__ __forceinline__ float moment1(float g, float m, const AdamCoef& c) { return fmaf(c.b1, m, c.omb1 * g); }
+__device__ __forceinline__ float moment2(float g, float v, const AdamCoef& c) {
+  return fmaf(c.b2, v, c.omb2 * (g * g));
+}
+
 __device__ __forceinline__ FwdOut fwd_elem(float p, float g, float m, float v, const AdamCoef& c) {
   FwdOut o;
-  o.m = fmaf(c.b1, m, c.omb1 * g);
-  o.v = fmaf(c.b2, v, c.omb2 * (g * g));
+  o.m = moment1(g, m, c);
+  o.v = moment2(g, v, c);
   const float s = sqrtf(fmaf(o.v, c.inv_c2, c.eps_root));
   const float d = s + c.eps;
   o.u = -(c.lr_c1 * o.m) / d;
@@ -84,8 +93,8 @@ struct BwdOut {
 template <bool HAS_MV>
 __device__ __forceinline__ BwdOut bwd_elem(float dP, float dM, float dV, float g, float m, float v,
                                            const AdamCoef& c) {
-  const float m1 = fmaf(c.b1, m, c.omb1 * g);
-  const float v1 = fmaf(c.b2, v, c.omb2 * (g * g));
+  const float m1 = moment1(g, m, c);
+  const float v1 = moment2(g, v, c);
   const float s = sqrtf(fmaf(v1, c.inv_c2, c.eps_root));
   const float d = s + c.eps;
   float kg, kvv;  // dupdate coefficients of dg and dv

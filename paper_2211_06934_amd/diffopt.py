@@ -20,6 +20,7 @@ DIFFOPT_OK = 0
 DIFFOPT_EINVAL = -1
 DIFFOPT_ENOMEM = -2
 DIFFOPT_EHIP = -3
+REMAT_SPAN = 8  # DIFFOPT_REMAT_SPAN: longest run of steps the K-step backward recomputes
 
 
 class DiffoptError(RuntimeError):
@@ -213,7 +214,11 @@ def adam_bwd(dupdate, dmu, dnu, grad, mu, nu, count, lr, b1, b2, eps, eps_root,
 
 def adam_unrolled_fwd(p0, grads, mu_traj, nu_traj, pK, count0, lr, b1, b2, eps, eps_root,
                       stream=None) -> None:
-    """diffopt_adam_unrolled_fwd; grads has K entries, mu_traj/nu_traj K+1."""
+    """diffopt_adam_unrolled_fwd; grads has K entries, mu_traj/nu_traj K+1.
+
+    Intermediate trajectory entries (0 < k < K) may be None: that state is not
+    stored, and adam_unrolled_bwd recomputes it (at most REMAT_SPAN - 1
+    consecutive None entries for the backward)."""
     K = len(grads)
     n = p0.numel()
     if len(mu_traj) != K + 1 or len(nu_traj) != K + 1:
@@ -226,7 +231,8 @@ def adam_unrolled_fwd(p0, grads, mu_traj, nu_traj, pK, count0, lr, b1, b2, eps, 
 
 def adam_unrolled_bwd(dpK, grads, mu_traj, nu_traj, dgrads, dmu0, dnu0, count0, lr, b1, b2, eps,
                       eps_root, stream=None) -> None:
-    """diffopt_adam_unrolled_bwd; mu_traj/nu_traj may hold K or K+1 entries."""
+    """diffopt_adam_unrolled_bwd; mu_traj/nu_traj may hold K or K+1 entries,
+    None where the forward did not store the state."""
     K = len(grads)
     n = dpK.numel()
     if len(dgrads) != K or len(mu_traj) < K or len(nu_traj) < K:

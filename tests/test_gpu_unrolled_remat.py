@@ -1,0 +1,186 @@
+"""The K-step driver with an incomplete moment trajectory.
+
+A caller may leave intermediate entries mu_traj[k], nu_traj[k] (1 <= k < K)
+NULL: the forward then does not store that state, and the backward recomputes
+it from the latest stored state before it, in registers, with the forward's
+own recurrences.  Recomputing is exact, so every output (p_K, the final state,
+every dg_k, dmu0, dnu0) and every state that is stored must equal the fully
+stored driver's bit for bit, whatever the store policy:
+
+  - nothing stored between the initial and final states (K <= 8);
+  - every 8th state (the longest recompute run);
+  - irregular policies whose unstored runs cross the forward's 16-step launch
+    boundaries (the running moments then pass through the final-state
+    buffers);
+  - ragged n (tail elements), misaligned buffers (element kernels) and an
+    in-place p_K == p0.
+
+The fully stored driver is itself checked against the oracle elsewhere; one
+case here also compares the recomputing run with the oracle directly.  Store
+policies the backward cannot serve are rejected before anything is enqueued.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.support import BWD_RTOL, FWD_RTOL, assert_mag_close, stats
+from tests.test_gpu_unrolled_fused import _assert_same, _inputs
+from workloads import HYPER, WORKLOADS, torch_normal
+
+pytestmark = pytest.mark.gpu
+
+LR, B1, B2, EPS = HYPER["lr"], HYPER["b1"], HYPER["b2"], HYPER["eps"]
+SPAN = 8  # DIFFOPT_REMAT_SPAN
+
+
+def _stored(policy, K):
+    """Indices 0..K of the states the caller stores (0 and K always)."""
+    if policy == "none":
+        keep = set()
+    elif policy == "all":
+        keep = set(range(K + 1))
+    elif isinstance(policy, int):
+        keep = set(range(0, K + 1, policy))
+    else:
+        keep = set(policy)
+    return keep | {0, K}
+
+
+def _run(p0, grads, m0, v0, cot, count0, er, policy, in_place=False, offset=0):
+    import paper_2211_06934_amd as P
+    K, n = len(grads), p0.numel()
+    keep = _stored(policy, K)
+
+    def buf(src=None):
+        t = torch.empty(n + offset, device="cuda")[offset:]
+        if src is not None:
+            t.copy_(src)
+        return t
+
+    p0b = buf(p0)
+    gb = [buf(x) for x in grads]
+    mt = [buf(m0)] + [buf() if k in keep else None for k in range(1, K + 1)]
+    vt = [buf(v0)] + [buf() if k in keep else None for k in range(1, K + 1)]
+    pK = p0b if in_place else buf()
+    P.adam_unrolled_fwd(p0b, gb, mt, vt, pK, count0, LR, B1, B2, EPS, er)
+    cb = buf(cot)
+    dg = [buf() for _ in range(K)]
+    dm0, dv0 = buf(), buf()
+    P.adam_unrolled_bwd(cb, gb, mt, vt, dg, dm0, dv0, count0, LR, B1, B2, EPS, er)
+    return pK, mt, vt, dg, dm0, dv0
+
+
+def _compare(got, ref, K):
+    _assert_same(got[0], ref[0], "p_K")
+    for k in range(1, K + 1):
+        if got[1][k] is not None:
+            _assert_same(got[1][k], ref[1][k], "mu_%d" % k)
+            _assert_same(got[2][k], ref[2][k], "nu_%d" % k)
+    for k in range(K):
+        _assert_same(got[3][k], ref[3][k], "dg_%d" % k)
+    _assert_same(got[4], ref[4], "dmu0")
+    _assert_same(got[5], ref[5], "dnu0")
+
+
+CASES = [  # K, n, count0, eps_root, nonzero initial state, store policy
+    (1, 4096, 0, 0.0, False, "none"),
+    (2, 5, 0, 0.0, False, "none"),
+    (3, 4097 * 4 + 3, 0, 1e-8, True, "none"),
+    (5, 12289, 7, 0.0, True, "none"),
+    (8, 1031, 0, 1e-8, False, "none"),          # one run of the maximum length
+    (9, 4096 * 3 + 1, 0, 0.0, True, 8),
+    (10, 777, 2, 1e-8, False, 8),
+    (12, 999, 0, 0.0, True, 2),                 # runs of two steps
+    (16, 12290, 0, 0.0, True, 8),
+    (17, 3001, 0, 1e-8, False, (3, 10)),        # state 16 unstored: carried across the launch boundary
+    (20, 5003, 1, 1e-8, True, 3),
+    (40, 2049, 0, 0.0, False, (7, 14, 21, 28, 35)),  # states 16 and 32 unstored
+    (33, 1025, 5, 0.0, True, (1, 2, 9, 10, 11, 18, 25, 32)),  # stored runs and recomputed runs mixed
+]
+
+
+@pytest.mark.parametrize("K,n,count0,er,nz,policy", CASES)
+def test_recomputed_trajectory_equals_stored_bitwise(K, n, count0, er, nz, policy):
+    inp = _inputs(K, n, K * 13 + n % 7, nz)
+    ref = _run(*inp, count0, er, "all")
+    got = _run(*inp, count0, er, policy)
+    torch.cuda.synchronize()
+    _compare(got, ref, K)
+
+
+@pytest.mark.parametrize("offset", [1, 4])
+@pytest.mark.parametrize("in_place", [False, True])
+def test_recomputed_misaligned_and_in_place(offset, in_place):
+    K, n = 6, 3 * 4096 + 5
+    inp = _inputs(K, n, 17, True)
+    ref = _run(*inp, 0, 1e-8, "all")
+    got = _run(*inp, 0, 1e-8, (2,), in_place=in_place, offset=offset)
+    torch.cuda.synchronize()
+    _compare(got, ref, K)
+
+
+def test_recomputed_run_against_oracle():
+    # no intermediate state stored; p_K, mu_K, nu_K and the meta-gradients
+    # against the all-fp64 oracle from the same fp32 inputs
+    K, n, count0, er = 8, 2 * 4096 + 11, 3, 1e-8
+    p0, grads, m0, v0, cot = _inputs(K, n, 29, True)
+    pK, mt, vt, dg, dm0, dv0 = _run(p0, grads, m0, v0, cot, count0, er, "none")
+    torch.cuda.synchronize()
+    h = lambda t: t.cpu().numpy().astype(np.float64)  # noqa: E731
+    hp0, hcot, hm0, hv0 = h(p0), h(cot), h(m0), h(v0)
+    hg = np.stack([h(x) for x in grads])
+    pK_ref, mt_ref, vt_ref = oracle.unrolled_fwd(hp0, hg, hm0, hv0, count0, LR, B1, B2, EPS, er)
+    mag_p = np.abs(hp0)
+    for k in range(1, K + 1):
+        mag_p = mag_p + oracle.adam_fwd_mag(hp0, hg[k - 1], mt_ref[k - 1], vt_ref[k - 1], count0 + k - 1,
+                                            LR, B1, B2, EPS, er)[3]
+    assert_mag_close(h(pK), pK_ref, mag_p, FWD_RTOL, "p_K")
+    for name, got, ref in (("mu_K", mt[K], mt_ref[K]), ("nu_K", vt[K], vt_ref[K])):
+        assert stats(h(got), ref)[1] < FWD_RTOL, name
+    _, dg_r, dm0_r, dv0_r = oracle.unrolled_bwd(hcot, hg, mt_ref, vt_ref, count0, LR, B1, B2, EPS, er)
+    worst = max([stats(h(dg[k]), dg_r[k])[1] for k in range(K)] + [stats(h(dm0), dm0_r)[1],
+                                                                     stats(h(dv0), dv0_r)[1]])
+    assert worst < BWD_RTOL, worst
+
+
+@pytest.mark.parametrize("name", ["many_small", "resnet18_k10"])
+def test_recomputed_full_size_equals_stored(name):
+    # the benchmark's shapes and launch configuration: nothing stored between
+    # the initial and final states (resnet18_k10: every 8th state)
+    w = WORKLOADS[name]()
+    K, n = w.K, w.n
+    p0 = torch_normal(n, 0.05, 1, "cuda")
+    grads = [torch_normal(n, w.grad_std, 10 + k, "cuda") for k in range(K)]
+    m0 = torch.zeros(n, device="cuda")
+    v0 = torch.zeros(n, device="cuda")
+    cot = torch_normal(n, 1.0, 3, "cuda")
+    policy = "none" if K <= SPAN else SPAN
+    got = _run(p0, grads, m0, v0, cot, w.count0, w.eps_root, policy)
+    ref = _run(p0, grads, m0, v0, cot, w.count0, w.eps_root, "all")
+    torch.cuda.synchronize()
+    _compare(got, ref, K)
+
+
+def test_store_policies_the_backward_cannot_serve_are_rejected():
+    import paper_2211_06934_amd as P
+    K, n = 10, 64
+    p0, grads, m0, v0, cot = _inputs(K, n, 3, False)
+    e = lambda: torch.empty(n, device="cuda")  # noqa: E731
+    mt = [m0] + [None] * (K - 1) + [e()]
+    vt = [v0] + [None] * (K - 1) + [e()]
+    pK = e()
+    # the forward itself does not need the states: nine unstored entries are fine
+    P.adam_unrolled_fwd(p0, grads, mt, vt, pK, 0, LR, B1, B2, EPS, 0.0)
+    dg = [e() for _ in range(K)]
+    with pytest.raises(P.DiffoptError, match="every 8-th state"):
+        P.adam_unrolled_bwd(cot, grads, mt, vt, dg, e(), e(), 0, LR, B1, B2, EPS, 0.0)
+    bad = list(vt)
+    bad[4] = e()  # nu stored where mu is not
+    with pytest.raises(P.DiffoptError, match="both be stored or both be NULL"):
+        P.adam_unrolled_fwd(p0, grads, mt, bad, pK, 0, LR, B1, B2, EPS, 0.0)
+    with pytest.raises(P.DiffoptError, match="final state"):
+        P.adam_unrolled_fwd(p0, grads, mt[:K] + [None], vt[:K] + [None], pK, 0, LR, B1, B2, EPS, 0.0)
+    with pytest.raises(P.DiffoptError, match="initial state"):
+        P.adam_unrolled_bwd(cot, grads, [None] + mt[1:], vt, dg, e(), e(), 0, LR, B1, B2, EPS, 0.0)
+    torch.cuda.synchronize()

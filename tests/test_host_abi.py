@@ -93,6 +93,36 @@ def test_validation_errors_before_any_device_call():
     assert "distinct" in d.last_error()
 
 
+def test_trajectory_store_policy_validation_on_host():
+    # intermediate moment states may be left unstored (NULL); every call below
+    # breaks a rule of the store policy and must fail before any device call
+    import paper_2211_06934_amd as P
+    d = P.diffopt
+    lib = d._lib
+    span = int(re.search(r"#define DIFFOPT_REMAT_SPAN (\d+)", open(HEADER).read()).group(1))
+    assert span == d.REMAT_SPAN
+    K = span + 2
+    f, f2 = ctypes.c_void_p(16), ctypes.c_void_p(32)
+    full = (ctypes.c_void_p * (K + 1))(*([16] * (K + 1)))
+    hole = (ctypes.c_void_p * (K + 1))(*([16] + [None] * (K - 1) + [16]))  # nothing stored between 0 and K
+    hyper = (0, 1e-3, .9, .999, 1e-8, 0.)
+    # backward: K - 1 > span - 1 consecutive unstored states
+    assert lib.diffopt_adam_unrolled_bwd(K, 8, f, full, hole, hole, full, f, f2, *hyper, None) == -1
+    assert "every %d-th state" % span in d.last_error()
+    # mu stored where nu is not
+    mixed = (ctypes.c_void_p * (K + 1))(*([16] * 3 + [None] * (K - 3) + [16]))
+    assert lib.diffopt_adam_unrolled_fwd(K, 8, f, full, full, mixed, f, *hyper, None) == -1
+    assert "both be stored or both be NULL" in d.last_error()
+    # the final state is required by the forward, the initial one by both
+    nolast = (ctypes.c_void_p * (K + 1))(*([16] * K + [None]))
+    assert lib.diffopt_adam_unrolled_fwd(K, 8, f, full, nolast, nolast, f, *hyper, None) == -1
+    assert "final state" in d.last_error()
+    nofirst = (ctypes.c_void_p * (K + 1))(*([None] + [16] * K))
+    assert lib.diffopt_adam_unrolled_bwd(K, 8, f, full, nofirst, nofirst, full, f, f2, *hyper, None) == -1
+    assert "initial state" in d.last_error()
+    assert lib.diffopt_adam_unrolled_fwd(K, 8, f, full, nofirst, nofirst, f, *hyper, None) == -1
+
+
 def test_segtable_validation_and_empty_tables_on_host():
     import paper_2211_06934_amd as P
     with pytest.raises(P.DiffoptError) as ei:
