@@ -48,16 +48,6 @@ TREE_UNROLL_CHUNK = 8  # the same for its leaf-direct form
 REMAT_SPAN = 8      # longest run of steps whose moments the backward recomputes
 
 
-def b_unrolled_fwd(K):
-    """K fused forward steps: p0, mu0, nu0 and K gradients in; K (mu, nu) and p_K out."""
-    return 16 + 12 * K
-
-
-def b_unrolled_bwd(K):
-    """K fused backward steps: dp_K and K (g, mu, nu) in; K dg and dmu0, dnu0 out."""
-    return 12 + 16 * K
-
-
 def stored_states(K, trajectory):
     """Indices 1..K of the moment states the forward stores: all of them, or
     (recompute) only the final one and every REMAT_SPAN-th."""
@@ -242,7 +232,7 @@ def phases_tree(S):
     ]
 
 
-def setup_treemap(torch, P, w):
+def setup_treemap(torch, P, w, trajectory):
     """Leaf-direct form of the same pass: every operand is a tree of separately
     allocated leaves; no flatten or unflatten."""
     from workloads import HYPER, torch_normal
@@ -266,8 +256,9 @@ def setup_treemap(torch, P, w):
     S["p0"] = tree(torch_normal(n, 0.05, 101, dev))
     S["g"] = [tree(torch_normal(n, w.grad_std, 110 + k, dev)) for k in range(K)]
     S["cot"] = tree(torch_normal(n, 1.0, 120, dev))
-    S["mu"] = [tree(zero=True)] + [tree() for _ in range(K)]
-    S["nu"] = [tree(zero=True)] + [tree() for _ in range(K)]
+    S["stored"] = stored = stored_states(K, trajectory)
+    S["mu"] = [tree(zero=True)] + [tree() if k in stored else None for k in range(1, K + 1)]
+    S["nu"] = [tree(zero=True)] + [tree() if k in stored else None for k in range(1, K + 1)]
     S["pK"] = tree()
     S["dg"] = [tree() for _ in range(K)]
     S["dm0"], S["dv0"] = tree(), tree()
@@ -291,8 +282,10 @@ def step_treemap(P, S, ev=None):
 
 def phases_treemap(S):
     K, n = S["K"], S["n"]
-    return [("adam_fwd_tree", "adam_unrolled_fwd_tree", -(-K // TREE_UNROLL_CHUNK), b_unrolled_fwd(K) * n),
-            ("adam_bwd_tree", "adam_unrolled_bwd_tree", -(-K // TREE_UNROLL_CHUNK), b_unrolled_bwd(K) * n)]
+    fl, fb = fwd_plan(K, S["stored"], TREE_UNROLL_CHUNK)
+    bl, bb = bwd_plan(K, S["stored"], TREE_UNROLL_CHUNK)
+    return [("adam_fwd_tree", "adam_unrolled_fwd_tree", fl, fb * n),
+            ("adam_bwd_tree", "adam_unrolled_bwd_tree", bl, bb * n)]
 
 
 def setup_flat_1b(torch, P, w):
@@ -511,7 +504,7 @@ def main():
     elif a.workload == "flat_1b":
         S, step, phases = setup_flat_1b(torch, P, w), step_flat_1b, phases_flat_1b
     elif a.workload == "many_small_treemap":
-        S, step, phases = setup_treemap(torch, P, w), step_treemap, phases_treemap
+        S, step, phases = setup_treemap(torch, P, w, a.trajectory), step_treemap, phases_treemap
     else:
         S, step, phases = setup_tree(torch, P, w, a.trajectory), step_tree, phases_tree
     ph = phases(S)

@@ -467,7 +467,7 @@ __global__ __launch_bounds__(kUBB) void adam_unrolled_bwd_elem(UBwdArgs a) {
 // dV: 8 in unless this run holds the last unrolled step, 8 out), against
 // 12 + 16C when every state is read back.  Registers hold 3C vectors, so a
 // run is at most kRS steps: the caller stores at least every kRS-th state.
-constexpr int kRS = DIFFOPT_REMAT_SPAN;
+constexpr int kRS = kRematSpan;
 constexpr int kURB = DIFFOPT_URBWD_BLOCK;
 
 // Step s of a run is unrolled step j+1+s (ascending); the VJP walks s = C-1..0.
@@ -487,9 +487,8 @@ struct URBwdArgs {
 template <int C>
 __device__ __forceinline__ void urbwd_vector(int64_t i, const URBwdArgs& a) {
   const f32x4 dP = ld(cv4(a.dP) + i);
-  f32x4 G[C], M[C], V[C];  // M[s], V[s]: the moments step s consumed
-  M[0] = ld(cv4(a.m0) + i);
-  V[0] = ld(cv4(a.v0) + i);
+  const f32x4 M0 = ld(cv4(a.m0) + i), V0 = ld(cv4(a.v0) + i);
+  f32x4 G[C];
 #pragma unroll
   for (int s = 0; s < C; ++s) G[s] = ld(cv4(a.g[s]) + i);
   f32x4 dM = {0.0f, 0.0f, 0.0f, 0.0f}, dV = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -497,6 +496,20 @@ __device__ __forceinline__ void urbwd_vector(int64_t i, const URBwdArgs& a) {
     dM = ld(cv4(a.dm) + i);
     dV = ld(cv4(a.dv) + i);
   }
+#if DIFFOPT_REMAT_QUAD_FLAT
+  // each VJP step recomputes its input moments from (M0, V0): C(C-1)/2
+  // moment steps instead of C - 1, and no trajectory held in registers
+#pragma unroll
+  for (int s = C - 1; s >= 0; --s) {
+    f32x4 M, V;
+    run_moments<C>(s, M0, V0, G, a.c, M, V);
+    if (s == C - 1 && !a.init_mv) ubwd_step<false>(dP, dM, dV, G[s], M, V, a.c[s], v4(a.dg[s]) + i);
+    else ubwd_step<true>(dP, dM, dV, G[s], M, V, a.c[s], v4(a.dg[s]) + i);
+  }
+#else
+  f32x4 M[C], V[C];  // M[s], V[s]: the moments step s consumed
+  M[0] = M0;
+  V[0] = V0;
 #pragma unroll
   for (int s = 0; s + 1 < C; ++s) {
 #pragma unroll
@@ -509,6 +522,7 @@ __device__ __forceinline__ void urbwd_vector(int64_t i, const URBwdArgs& a) {
   else ubwd_step<false>(dP, dM, dV, G[C - 1], M[C - 1], V[C - 1], a.c[C - 1], v4(a.dg[C - 1]) + i);
 #pragma unroll
   for (int s = C - 2; s >= 0; --s) ubwd_step<true>(dP, dM, dV, G[s], M[s], V[s], a.c[s], v4(a.dg[s]) + i);
+#endif
   st(v4(a.dm) + i, dM);
   st(v4(a.dv) + i, dV);
 }
@@ -692,35 +706,6 @@ extern "C" int diffopt_adam_bwd(const float* dupdate, const float* dmu, const fl
     if (!aligned4(q)) return fail(DIFFOPT_EINVAL, "diffopt_adam_bwd: pointer %p is not 4-byte aligned", q);
   return launch_bwd(dupdate, dmu, dnu, grad, mu, nu, n, c, dparams, dgrad, dmu_in, dnu_in, as_stream(stream));
 }
-
-namespace diffopt {
-namespace {
-
-// Stored-state bookkeeping shared by both drivers: entry k (1..K-1) of a
-// trajectory may be NULL (not stored), mu and nu together.  The backward
-// (bound_runs) recomputes a NULL state from the latest stored one before it,
-// in registers, so at most kRS - 1 consecutive entries may be NULL.
-int check_trajectory(const char* who, int64_t K, const float* const* mu_traj, const float* const* nu_traj,
-                     bool need_last, bool bound_runs) {
-  if (!mu_traj[0] || !nu_traj[0]) return fail(DIFFOPT_EINVAL, "%s: null initial state mu_traj[0] / nu_traj[0]", who);
-  if (need_last && (!mu_traj[K] || !nu_traj[K]))
-    return fail(DIFFOPT_EINVAL, "%s: null final state mu_traj[K] / nu_traj[K]", who);
-  int64_t last = 0;  // latest stored state
-  for (int64_t k = 1; k < K; ++k) {
-    if ((mu_traj[k] == nullptr) != (nu_traj[k] == nullptr))
-      return fail(DIFFOPT_EINVAL, "%s: trajectory entry %lld: mu and nu must both be stored or both be NULL", who,
-                  (long long)k);
-    if (mu_traj[k]) last = k;
-    else if (bound_runs && k + 1 - last > kRS)
-      return fail(DIFFOPT_EINVAL,
-                  "%s: trajectory entries %lld..%lld are all NULL; at least every %d-th state must be stored", who,
-                  (long long)(last + 1), (long long)k, kRS);
-  }
-  return DIFFOPT_OK;
-}
-
-}  // namespace
-}  // namespace diffopt
 
 extern "C" int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0, const float* const* grads,
                                          float* const* mu_traj, float* const* nu_traj, float* pK, int64_t count0,

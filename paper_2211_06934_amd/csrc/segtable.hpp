@@ -34,6 +34,20 @@ constexpr int64_t kTileGroups = (int64_t)kTB * kTreeU;
 constexpr int64_t kLeafGroupAlign = 8;
 constexpr int kWindowMax = (int)(kTileGroups / kLeafGroupAlign + 2);
 
+// Leaf and flat-buffer memory is device (global) memory, but its addresses
+// come from the staged LDS window as integers, so a plain pointer would be
+// generic and every access a flat_* instruction.  Flat instructions count
+// against the LDS wait counter too: a lane's next window lookup would then
+// wait for all of its outstanding HBM loads.  Address space 1 makes the
+// compiler emit global_* instructions, which count only as vector memory.
+template <typename T>
+using gptr = __attribute__((address_space(1))) T*;
+
+template <typename T>
+__device__ __forceinline__ gptr<T> gaddr(uint64_t addr) {
+  return (gptr<T>)addr;
+}
+
 // One nonempty leaf, in table order.  The entry after the last nonempty leaf
 // is a sentinel whose goff is the total group count.
 struct SegEntry {

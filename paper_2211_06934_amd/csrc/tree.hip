@@ -154,7 +154,7 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
           kind[u] = 1;
           const uint64_t S = A + delta[u];
           shift[u] = (uint32_t)(S & 15u);
-          const u32x4* L = reinterpret_cast<const u32x4*>(S - shift[u]);
+          const gptr<const u32x4> L = gaddr<const u32x4>(S - shift[u]);
 #if DIFFOPT_TREE_NT_LOADS
           w0[u] = __builtin_nontemporal_load(L);
           if (shift[u] != 0) w1[u] = __builtin_nontemporal_load(L + 1);
@@ -174,13 +174,13 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
     if (kind[u] == 1) {
       const u32x4 out = shift[u] != 0 ? funnel<E>(w0[u], w1[u], shift[u]) : w0[u];
 #if DIFFOPT_TREE_NT_STORES
-      __builtin_nontemporal_store(out, reinterpret_cast<u32x4*>(dst[u]));
+      __builtin_nontemporal_store(out, gaddr<u32x4>(dst[u]));
 #else
-      *reinterpret_cast<u32x4*>(dst[u]) = out;
+      *gaddr<u32x4>(dst[u]) = out;
 #endif
     } else if (kind[u] == 2) {
       for (uint64_t x = lo_b[u]; x < hi_b[u]; x += E) {
-        *reinterpret_cast<T*>(x) = *reinterpret_cast<const T*>(x + delta[u]);
+        *gaddr<T>(x) = *gaddr<const T>(x + delta[u]);
       }
     }
   }

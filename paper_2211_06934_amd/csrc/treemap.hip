@@ -82,8 +82,8 @@ __device__ __forceinline__ int find_leaf(const int64_t* s_goff, int W, int64_t g
 }
 
 template <typename T>
-__device__ __forceinline__ T* at(uint64_t base, int64_t i) {
-  return reinterpret_cast<T*>(base) + i;
+__device__ __forceinline__ gptr<T> at(uint64_t base, int64_t i) {
+  return gaddr<T>(base) + i;
 }
 
 // Operands: 0 p, 1 g, 2 m, 3 v (inputs); 4 p', 5 m', 6 v' (outputs).
@@ -260,24 +260,27 @@ struct TBwdArgs {
 
 // Stage the window of tile b for `na` operand trees: (operand, leaf) pairs
 // are spread over the workgroup, then each leaf's all-operands-aligned flag
-// is formed from LDS.  Ends with the workgroup synchronised.
+// is formed from LDS.  A NULL operand (a trajectory state the caller does
+// not store) stages address 0 and is never dereferenced.  Ends with the
+// workgroup synchronised.
+template <int NT = kUTB>
 __device__ __forceinline__ int stage_window_n(const SegEntry* __restrict__ seg, const int64_t* __restrict__ tile_first,
                                               const uint64_t* const* arrs, int na, int dense_orig, int64_t b,
                                               int64_t* s_goff, int64_t* s_numel, uint64_t* s_ptr, int* s_al) {
   const int64_t j0 = tile_first[b];
   const int W = (int)(tile_first[b + 1] - j0 + 1);
-  for (int t = threadIdx.x; t <= W; t += kUTB) {
+  for (int t = threadIdx.x; t <= W; t += NT) {
     const SegEntry e = seg[j0 + t];
     s_goff[t] = e.goff;
     if (t < W) s_numel[t] = e.numel;
   }
-  for (int x = threadIdx.x; x < W * na; x += kUTB) {
+  for (int x = threadIdx.x; x < W * na; x += NT) {
     const int q = x / W, t = x - q * W;
     const int64_t leaf = dense_orig ? j0 + t : seg[j0 + t].orig;
-    s_ptr[q * kWindowMax + t] = arrs[q][leaf];
+    s_ptr[q * kWindowMax + t] = arrs[q] ? arrs[q][leaf] : 0;  // NULL operand: an unstored state
   }
   __syncthreads();
-  for (int t = threadIdx.x; t < W; t += kUTB) {
+  for (int t = threadIdx.x; t < W; t += NT) {
     uint64_t any = 0;
     for (int q = 0; q < na; ++q) any |= s_ptr[q * kWindowMax + t];
     s_al[t] = (any & 15u) == 0;
@@ -318,8 +321,10 @@ __global__ __launch_bounds__(kUTB) void adam_unrolled_fwd_tree_kernel(const SegE
         m[e] = o.m;
         v[e] = o.v;
       }
-      st(at<f32x4>(OP(5 + 3 * s), i), m);
-      st(at<f32x4>(OP(6 + 3 * s), i), v);
+      if (a.a[5 + 3 * s]) {  // uniform: a stored state
+        st(at<f32x4>(OP(5 + 3 * s), i), m);
+        st(at<f32x4>(OP(6 + 3 * s), i), v);
+      }
       g = gn;
     }
     st(at<f32x4>(OP(3), i), p);
@@ -332,8 +337,10 @@ __global__ __launch_bounds__(kUTB) void adam_unrolled_fwd_tree_kernel(const SegE
         p = o.p;
         m = o.m;
         v = o.v;
-        *at<float>(OP(5 + 3 * s), i) = m;
-        *at<float>(OP(6 + 3 * s), i) = v;
+        if (a.a[5 + 3 * s]) {
+          *at<float>(OP(5 + 3 * s), i) = m;
+          *at<float>(OP(6 + 3 * s), i) = v;
+        }
       }
       *at<float>(OP(3), i) = p;
     }
@@ -425,6 +432,164 @@ __global__ __launch_bounds__(kUTB) void adam_unrolled_bwd_tree_kernel(const SegE
 #undef OP
 }
 
+// ---- fused VJP over a run of steps whose moments were not stored ----------------
+// Leaf-direct form of the flat driver's recomputing VJP: for a run of C steps
+// j+1..j+C with only (mu_j, nu_j) stored, each lane reads that state and the
+// C gradients of its group once, recomputes the run's moments in registers
+// with the forward's recurrences, then walks the C VJP steps last first.
+constexpr int kTRS = kRematSpan;
+constexpr int kTRBwdNA = 5 + 2 * kTRS;  // 0 dP, 1 dmu, 2 dnu, 3 mu_j, 4 nu_j; per step s: 5+2s g, 6+2s dg
+
+// Step s of a run is unrolled step j+1+s (ascending).
+struct TRBwdArgs {
+  const uint64_t* a[kTRBwdNA];
+  AdamCoef c[kTRS];
+  int32_t init_mv;  // 0: the run holds the last unrolled step (zero dM, dV before it)
+};
+
+// Workgroups per table tile: each stages the tile's whole window and takes
+// its share of the tile's groups, one per lane.  With its register count
+// (78 VGPRs at C = 3) a CU holds two 512-thread workgroups but five of 256
+// threads; measured on MI355X (K = 3, 20,000 leaves) the split of 2 runs at
+// 5.46 TB/s against 5.27 unsplit (4: 5.50, within noise).
+#ifndef DIFFOPT_TRBWD_SPLIT
+#define DIFFOPT_TRBWD_SPLIT 2
+#endif
+constexpr int kTRSplit = DIFFOPT_TRBWD_SPLIT;
+constexpr int kTRB = kUTB / kTRSplit;
+static_assert(kUTB % kTRSplit == 0, "the split must divide the tile");
+
+template <int C>
+__global__ __launch_bounds__(kTRB) void adam_unrolled_bwd_tree_remat_kernel(const SegEntry* __restrict__ seg,
+                                                                           const int64_t* __restrict__ tile_first,
+                                                                           int64_t ngroups, int dense_orig,
+                                                                           TRBwdArgs a) {
+  __shared__ int64_t s_goff[kWindowMax + 1];
+  __shared__ int64_t s_numel[kWindowMax];
+  __shared__ int s_al[kWindowMax];
+  extern __shared__ uint64_t s_ptr[];  // [na][kWindowMax]
+  constexpr int na = 5 + 2 * C;
+  const int64_t b = blockIdx.x / kTRSplit;  // table tile
+  const int W = stage_window_n<kTRB>(seg, tile_first, a.a, na, dense_orig, b, s_goff, s_numel, s_ptr, s_al);
+  const int64_t gidx = b * kTileGroups + (int64_t)(blockIdx.x % kTRSplit) * kTRB + threadIdx.x;
+  if (gidx >= ngroups) return;
+  const int t = find_leaf(s_goff, W, gidx);
+  const int64_t e0 = 4 * (gidx - s_goff[t]);
+  const int64_t nel = s_numel[t];
+  if (e0 >= nel) return;
+  const uint64_t* P = s_ptr + t;
+#define OP(q) P[(q) * kWindowMax]
+  if (e0 + 4 <= nel && s_al[t]) {
+    const int64_t i = e0 >> 2;
+    const f32x4 dP = ld(at<const f32x4>(OP(0), i));
+    const f32x4 M0 = ld(at<const f32x4>(OP(3), i)), V0 = ld(at<const f32x4>(OP(4), i));
+    f32x4 G[C];
+#pragma unroll
+    for (int s = 0; s < C; ++s) G[s] = ld(at<const f32x4>(OP(5 + 2 * s), i));
+    f32x4 dM = {0.0f, 0.0f, 0.0f, 0.0f}, dV = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (a.init_mv) {
+      dM = ld(at<const f32x4>(OP(1), i));
+      dV = ld(at<const f32x4>(OP(2), i));
+    }
+#if !DIFFOPT_REMAT_QUAD_TREE
+    f32x4 M[C], V[C];  // M[s], V[s]: the moments step s consumed
+    M[0] = M0;
+    V[0] = V0;
+#pragma unroll
+    for (int s = 0; s + 1 < C; ++s) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        M[s + 1][e] = moment1(G[s][e], M[s][e], a.c[s]);
+        V[s + 1][e] = moment2(G[s][e], V[s][e], a.c[s]);
+      }
+    }
+#endif
+#pragma unroll
+    for (int s = C - 1; s >= 0; --s) {
+#if DIFFOPT_REMAT_QUAD_TREE
+      f32x4 Ms, Vs;  // this step's input moments, recomputed from (M0, V0)
+      run_moments<C>(s, M0, V0, G, a.c, Ms, Vs);
+#else
+      const f32x4 Ms = M[s], Vs = V[s];
+#endif
+      f32x4 rg;
+      if (s == C - 1 && !a.init_mv) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const BwdOut o = bwd_elem<false>(dP[e], 0.0f, 0.0f, G[s][e], Ms[e], Vs[e], a.c[s]);
+          rg[e] = o.g;
+          dM[e] = o.m;
+          dV[e] = o.v;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const BwdOut o = bwd_elem<true>(dP[e], dM[e], dV[e], G[s][e], Ms[e], Vs[e], a.c[s]);
+          rg[e] = o.g;
+          dM[e] = o.m;
+          dV[e] = o.v;
+        }
+      }
+      st(at<f32x4>(OP(6 + 2 * s), i), rg);
+    }
+    st(at<f32x4>(OP(1), i), dM);
+    st(at<f32x4>(OP(2), i), dV);
+  } else {
+    const int64_t end = e0 + 4 < nel ? e0 + 4 : nel;
+    for (int64_t i = e0; i < end; ++i) {
+      const float dP = *at<const float>(OP(0), i);
+      float G[C], M[C], V[C];
+      M[0] = *at<const float>(OP(3), i);
+      V[0] = *at<const float>(OP(4), i);
+#pragma unroll
+      for (int s = 0; s < C; ++s) G[s] = *at<const float>(OP(5 + 2 * s), i);
+#pragma unroll
+      for (int s = 0; s + 1 < C; ++s) {
+        M[s + 1] = moment1(G[s], M[s], a.c[s]);
+        V[s + 1] = moment2(G[s], V[s], a.c[s]);
+      }
+      float dM = 0.0f, dV = 0.0f;
+      if (a.init_mv) {
+        dM = *at<const float>(OP(1), i);
+        dV = *at<const float>(OP(2), i);
+      }
+#pragma unroll
+      for (int s = C - 1; s >= 0; --s) {
+        const BwdOut o = (s == C - 1 && !a.init_mv) ? bwd_elem<false>(dP, 0.0f, 0.0f, G[s], M[s], V[s], a.c[s])
+                                                    : bwd_elem<true>(dP, dM, dV, G[s], M[s], V[s], a.c[s]);
+        *at<float>(OP(6 + 2 * s), i) = o.g;
+        dM = o.m;
+        dV = o.v;
+      }
+      *at<float>(OP(1), i) = dM;
+      *at<float>(OP(2), i) = dV;
+    }
+  }
+#undef OP
+}
+
+template <int C>
+void launch_trbwd(const diffopt_segtable* t, const TRBwdArgs& a, hipStream_t st) {
+  const size_t lds = sizeof(uint64_t) * kWindowMax * (5 + 2 * C);
+  hipLaunchKernelGGL((adam_unrolled_bwd_tree_remat_kernel<C>), dim3((unsigned)(t->ntiles * kTRSplit)), dim3(kTRB),
+                     lds, st, t->d_seg, t->d_tile_first, t->ngroups, t->dense_orig, a);
+}
+
+// Run length C is a template argument so the trajectory stays in registers.
+void launch_trbwd_c(int C, const diffopt_segtable* t, const TRBwdArgs& a, hipStream_t st) {
+  switch (C) {
+    case 1: launch_trbwd<1>(t, a, st); break;
+    case 2: launch_trbwd<2>(t, a, st); break;
+    case 3: launch_trbwd<3>(t, a, st); break;
+    case 4: launch_trbwd<4>(t, a, st); break;
+    case 5: launch_trbwd<5>(t, a, st); break;
+    case 6: launch_trbwd<6>(t, a, st); break;
+    case 7: launch_trbwd<7>(t, a, st); break;
+    default: launch_trbwd<8>(t, a, st); break;
+  }
+}
+static_assert(kTRS == 8, "launch_trbwd_c instantiates run lengths 1..8");
+
 int check_table(const char* who, const diffopt_segtable* t) {
   if (!t) return fail(DIFFOPT_EINVAL, "%s: table is NULL", who);
   if (t->elem_bytes != 4) return fail(DIFFOPT_EINVAL, "%s: the table must describe fp32 leaves (elem_bytes 4)", who);
@@ -514,23 +679,29 @@ extern "C" int diffopt_adam_unrolled_fwd_tree(const diffopt_segtable* table, int
   }
   if (table->ntiles == 0) return DIFFOPT_OK;
   if (!p0 || !pK) return fail(DIFFOPT_EINVAL, "%s: null p0 or pK", who);
-  for (int64_t k = 0; k <= K; ++k) {
-    if (!mu_traj[k] || !nu_traj[k]) return fail(DIFFOPT_EINVAL, "%s: null trajectory entry %lld", who, (long long)k);
-    if (k < K && !grads[k]) return fail(DIFFOPT_EINVAL, "%s: null grads entry %lld", who, (long long)k);
-  }
+  for (int64_t k = 0; k < K; ++k)
+    if (!grads[k]) return fail(DIFFOPT_EINVAL, "%s: null grads entry %lld", who, (long long)k);
+  rc = check_trajectory(who, K, mu_traj, nu_traj, true, false);
+  if (rc) return rc;
   hipStream_t st = as_stream(stream);
   for (int64_t k0 = 0; k0 < K; k0 += kTK) {  // one fused launch per kTK steps
     TFwdArgs a{};
     a.K = (int32_t)(K - k0 < kTK ? K - k0 : kTK);
+    // between launches the running moments pass through the state stored at
+    // the boundary, or through the final-state trees when it is not stored
     a.a[0] = (k0 == 0) ? p0 : pK;
-    a.a[1] = mu_traj[k0];
-    a.a[2] = nu_traj[k0];
+    a.a[1] = mu_traj[k0] ? mu_traj[k0] : mu_traj[K];
+    a.a[2] = nu_traj[k0] ? nu_traj[k0] : nu_traj[K];
     a.a[3] = pK;
     for (int s = 0; s < a.K; ++s) {
       a.a[4 + 3 * s] = grads[k0 + s];
       a.a[5 + 3 * s] = mu_traj[k0 + s + 1];
       a.a[6 + 3 * s] = nu_traj[k0 + s + 1];
       make_coef(who, count0 + k0 + s, lr, b1, b2, eps, eps_root, &a.c[s]);
+    }
+    if (!a.a[5 + 3 * (a.K - 1)]) {
+      a.a[5 + 3 * (a.K - 1)] = mu_traj[K];
+      a.a[6 + 3 * (a.K - 1)] = nu_traj[K];
     }
     const size_t lds = sizeof(uint64_t) * kWindowMax * (4 + 3 * a.K);
     hipLaunchKernelGGL(adam_unrolled_fwd_tree_kernel, dim3((unsigned)table->ntiles), dim3(kUTB), lds, st,
@@ -560,29 +731,57 @@ extern "C" int diffopt_adam_unrolled_bwd_tree(const diffopt_segtable* table, int
   if (table->ntiles == 0) return DIFFOPT_OK;
   if (!dpK || !dmu0 || !dnu0) return fail(DIFFOPT_EINVAL, "%s: null dpK, dmu0 or dnu0", who);
   if (dmu0 == dnu0) return fail(DIFFOPT_EINVAL, "%s: dmu0 and dnu0 must be distinct", who);
-  for (int64_t k = 0; k < K; ++k) {
-    if (!grads[k] || !mu_traj[k] || !nu_traj[k] || !dgrads[k])
-      return fail(DIFFOPT_EINVAL, "%s: null entry %lld in a pointer array", who, (long long)k);
-  }
+  for (int64_t k = 0; k < K; ++k)
+    if (!grads[k] || !dgrads[k])
+      return fail(DIFFOPT_EINVAL, "%s: null entry %lld in grads or dgrads", who, (long long)k);
+  rc = check_trajectory(who, K, mu_traj, nu_traj, false, true);
+  if (rc) return rc;
   hipStream_t st = as_stream(stream);
-  for (int64_t khi = K; khi >= 1; khi -= kTK) {  // one fused launch per kTK steps, last steps first
-    TBwdArgs a{};
-    a.K = (int32_t)(khi < kTK ? khi : kTK);
-    a.init_mv = khi != K;  // the first launch starts from zero cotangents of mu_K, nu_K
-    a.a[0] = dpK;
-    a.a[1] = dmu0;
-    a.a[2] = dnu0;
-    for (int s = 0; s < a.K; ++s) {
-      const int64_t k = khi - s;  // unrolled step (1-based) run as the launch's step s
-      a.a[3 + 4 * s] = grads[k - 1];
-      a.a[4 + 4 * s] = mu_traj[k - 1];
-      a.a[5 + 4 * s] = nu_traj[k - 1];
-      a.a[6 + 4 * s] = dgrads[k - 1];
-      make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &a.c[s]);
+  // Last steps first: runs of steps whose input states are stored take one
+  // launch per kTK steps; a run j+1..khi after one stored state j takes one
+  // launch that recomputes the states it needs.
+  for (int64_t khi = K; khi >= 1;) {
+    const int32_t init_mv = khi != K;  // the first launch starts from zero cotangents of mu_K, nu_K
+    if (mu_traj[khi - 1]) {
+      TBwdArgs a{};
+      int32_t run = 0;
+      while (run < kTK && khi - run >= 1 && mu_traj[khi - run - 1]) ++run;
+      a.K = run;
+      a.init_mv = init_mv;
+      a.a[0] = dpK;
+      a.a[1] = dmu0;
+      a.a[2] = dnu0;
+      for (int s = 0; s < a.K; ++s) {
+        const int64_t k = khi - s;  // unrolled step (1-based) run as the launch's step s
+        a.a[3 + 4 * s] = grads[k - 1];
+        a.a[4 + 4 * s] = mu_traj[k - 1];
+        a.a[5 + 4 * s] = nu_traj[k - 1];
+        a.a[6 + 4 * s] = dgrads[k - 1];
+        make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &a.c[s]);
+      }
+      const size_t lds = sizeof(uint64_t) * kWindowMax * (3 + 4 * a.K);
+      hipLaunchKernelGGL(adam_unrolled_bwd_tree_kernel, dim3((unsigned)table->ntiles), dim3(kUTB), lds, st,
+                         table->d_seg, table->d_tile_first, table->ngroups, table->dense_orig, a);
+      khi -= run;
+    } else {
+      int64_t j = khi - 1;
+      while (!mu_traj[j]) --j;  // mu_traj[0] is stored; check_trajectory bounds khi - j by kTRS
+      const int C = (int)(khi - j);
+      TRBwdArgs a{};
+      a.init_mv = init_mv;
+      a.a[0] = dpK;
+      a.a[1] = dmu0;
+      a.a[2] = dnu0;
+      a.a[3] = mu_traj[j];
+      a.a[4] = nu_traj[j];
+      for (int s = 0; s < C; ++s) {
+        a.a[5 + 2 * s] = grads[j + s];
+        a.a[6 + 2 * s] = dgrads[j + s];
+        make_coef(who, count0 + j + s, lr, b1, b2, eps, eps_root, &a.c[s]);
+      }
+      launch_trbwd_c(C, table, a, st);
+      khi = j;
     }
-    const size_t lds = sizeof(uint64_t) * kWindowMax * (3 + 4 * a.K);
-    hipLaunchKernelGGL(adam_unrolled_bwd_tree_kernel, dim3((unsigned)table->ntiles), dim3(kUTB), lds, st,
-                       table->d_seg, table->d_tile_first, table->ngroups, table->dense_orig, a);
     rc = launch_status(who);
     if (rc) return rc;
   }
