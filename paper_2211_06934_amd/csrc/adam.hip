@@ -26,17 +26,20 @@
 #ifndef DIFFOPT_ADAM_BLOCK
 #define DIFFOPT_ADAM_BLOCK 1024  // threads per workgroup of the Adam kernels
 #endif
-// Fused K-step kernels, measured in the many-small step (K = 3): the forward
-// is fastest at 256 threads (1.06 ms against 1.07 at 512 and 1024), the VJP at
-// 1024 (1.20 ms against 1.25 at 512 and 1.26 at 256).
+// Fused K-step kernels, measured in the many-small step (K = 3).  Forward
+// storing only the final state: 1024 threads 0.695 ms, 512 0.710, 256 0.731
+// (with the whole trajectory stored the three were within 1%).  VJP reading
+// the whole trajectory: 1024 threads 1.20 ms against 1.25 at 512 and 1.26 at
+// 256.  VJP recomputing the moments: 512 threads 0.859 ms, 256 0.880, 1024
+// 0.901.
 #ifndef DIFFOPT_UFWD_BLOCK
-#define DIFFOPT_UFWD_BLOCK 256  // threads per workgroup, fused K-step forward
+#define DIFFOPT_UFWD_BLOCK 1024  // threads per workgroup, fused K-step forward
 #endif
 #ifndef DIFFOPT_UBWD_BLOCK
 #define DIFFOPT_UBWD_BLOCK 1024  // threads per workgroup, fused K-step VJP
 #endif
 #ifndef DIFFOPT_URBWD_BLOCK
-#define DIFFOPT_URBWD_BLOCK 256  // threads per workgroup, fused VJP recomputing the moments
+#define DIFFOPT_URBWD_BLOCK 512  // threads per workgroup, fused VJP recomputing the moments
 #endif
 
 namespace diffopt {
