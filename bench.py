@@ -597,7 +597,11 @@ def main():
                             "many_small_treemap": "leaf-direct K-step Adam fwd -> K-step Adam bwd (no flatten)"}.get(
                                 a.workload,
                                 "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg"),
-                   "launch": "hip graph replay" if a.graph else "eager", "parallelism": "single GPU"},
+                   "launch": "hip graph replay" if a.graph else "eager", "parallelism": "single GPU",
+                   **({"trajectory": {"recompute": "final moment state stored (and every %d-th); the VJP recomputes "
+                                                   "the rest" % REMAT_SPAN,
+                                      "stored": "every moment state stored"}[a.trajectory]}
+                      if "stored" in S else {})},
         "us_per_step": round(ms_step * 1e3, 2),
         "achieved_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
         "bytes_per_step": int(bytes_step), "phases": breakdown,

@@ -1,0 +1,54 @@
+"""CPU checks of bench.py's byte accounting: the interface bytes per element
+that the K-step driver must move under each store policy, derived here by
+hand from what each launch reads and writes (fp32, 4 bytes per array)."""
+import importlib.util
+import os
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _bench():
+    spec = importlib.util.spec_from_file_location("bench_under_test", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_whole_trajectory_one_launch():
+    b = _bench()
+    for K in (1, 3, 5, 16):
+        st = b.stored_states(K, "stored")
+        # forward: p0, mu0, nu0 and K g in; K (mu, nu) and p_K out
+        assert b.fwd_plan(K, st, 16) == (1, 16 + 12 * K)
+        # VJP: dP and K (g, mu, nu) in; K dg and dmu0, dnu0 out
+        assert b.bwd_plan(K, st, 16) == (1, 12 + 16 * K)
+
+
+def test_recomputed_trajectory_one_launch():
+    b = _bench()
+    for K in (1, 3, 8):
+        st = b.stored_states(K, "recompute")
+        assert st == {K}
+        # forward: p0, mu0, nu0, K g in; p_K, mu_K, nu_K out
+        assert b.fwd_plan(K, st, 16) == (1, 24 + 4 * K)
+        # VJP: dP, mu0, nu0, K g in; K dg, dmu0, dnu0 out
+        assert b.bwd_plan(K, st, 16) == (1, 20 + 8 * K)
+
+
+def test_launch_boundaries():
+    b = _bench()
+    # K = 10, recompute: state 8 stored as well.  Forward: one launch, two
+    # states out.  VJP: run (8, 10] reads state 8 (no running dM, dV in), run
+    # (0, 8] reads state 0 and the running dM, dV.
+    st = b.stored_states(10, "recompute")
+    assert st == {8, 10}
+    assert b.fwd_plan(10, st, 16) == (1, 16 + 40 + 16)
+    assert b.bwd_plan(10, st, 16) == (2, (4 + 8 + 8 + 2 * 8) + (4 + 8 + 8 + 8 + 8 * 8))
+    # K = 17, whole trajectory: two forward launches (16 + 1 steps), p, mu, nu
+    # re-read and p re-written at the boundary; two VJP launches, the second
+    # reading the running dM, dV.
+    st = b.stored_states(17, "stored")
+    assert b.fwd_plan(17, st, 16) == (2, (16 + 16 * 4 + 16 * 8) + (16 + 4 + 8))
+    assert b.bwd_plan(17, st, 16) == (2, (4 + 8 + 16 * 16) + (4 + 8 + 8 + 16))
+    # the leaf-direct driver launches every 8 steps
+    assert b.fwd_plan(9, b.stored_states(9, "stored"), 8)[0] == 2
