@@ -13,6 +13,8 @@ fix an order; any fixed order works as long as flatten and unflatten agree.
 """
 from __future__ import annotations
 
+import contextlib
+
 import dataclasses
 from typing import Any, Dict, List, Optional, Sequence, Tuple
 
@@ -113,13 +115,28 @@ def segment_table(shapes: Sequence[Tuple[int, ...]], dtype: torch.dtype,
     return t
 
 
-def leaf_pointer_tensor(leaves: Sequence[torch.Tensor], device) -> torch.Tensor:
-    """Device int64 array of leaf addresses, in table order."""
+def _stream_context(stream):
+    """Make `stream` (a torch stream, a raw hipStream_t address or None) current."""
+    if stream is None:
+        return contextlib.nullcontext()
+    if isinstance(stream, int):
+        stream = torch.cuda.ExternalStream(stream)
+    return torch.cuda.stream(stream)
+
+
+def leaf_pointer_tensor(leaves: Sequence[torch.Tensor], device, stream=None) -> torch.Tensor:
+    """Device int64 array of leaf addresses, in table order.
+
+    It is allocated on `stream` (default: the current one), the stream whose
+    kernel reads it: torch's caching allocator hands a freed block only to
+    later work on the stream it was allocated on, so the array may be dropped
+    as soon as the kernel is enqueued."""
     for i, x in enumerate(leaves):
         if not x.is_contiguous():
             raise ValueError("leaf %d is not contiguous" % i)
     ptrs = [x.data_ptr() for x in leaves]
-    return torch.tensor(ptrs, dtype=torch.int64).to(device, non_blocking=False)
+    with _stream_context(stream):
+        return torch.tensor(ptrs, dtype=torch.int64).to(device, non_blocking=False)
 
 
 def flatten(tree, out: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, FlatSpec]:
@@ -138,7 +155,7 @@ def flatten(tree, out: Optional[torch.Tensor] = None, stream=None) -> Tuple[torc
         out = torch.empty(table.total, dtype=dtype, device=device)
     elif out.numel() < table.total or out.dtype != dtype:
         raise ValueError("out is too small or of the wrong dtype")
-    _d.tree_flatten(table, leaf_pointer_tensor(leaves, device), out, stream)
+    _d.tree_flatten(table, leaf_pointer_tensor(leaves, device, stream), out, stream)
     return out, FlatSpec(td, shapes, dtype, table)
 
 
@@ -147,5 +164,5 @@ def unflatten(flat: torch.Tensor, spec: FlatSpec, out_leaves: Optional[Sequence[
     """Split a flat buffer into new (or given) leaf tensors and rebuild the tree."""
     if out_leaves is None:
         out_leaves = [torch.empty(s, dtype=spec.dtype, device=flat.device) for s in spec.shapes]
-    _d.tree_unflatten(spec.table, flat, leaf_pointer_tensor(out_leaves, flat.device), stream)
+    _d.tree_unflatten(spec.table, flat, leaf_pointer_tensor(out_leaves, flat.device, stream), stream)
     return tree_build(spec.treedef, out_leaves)

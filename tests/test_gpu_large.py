@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import oracle
-from tests.support import BWD_RTOL, FWD_RTOL, assert_bits_equal, assert_mag_close
+from tests.support import BWD_RTOL, FWD_RTOL, assert_bits_equal, assert_mag_close, stats
 from tests.test_gpu_unrolled import _check_unrolled
 from workloads import HYPER, torch_normal
 
@@ -190,3 +190,75 @@ def test_es_rows_past_2_31_elements():
     scale = 1.0 / (2 * N * sigma)
     assert_mag_close(_take(g, ti), oracle.es_estimate(hz, hw, scale), oracle.es_estimate_mag(hz, hw, scale),
                      BWD_RTOL, "estimate")
+
+
+def _end_to_end(h_p0, hG, h_cot, got_pK, got_muK, got_nuK, got_dg, got_dm0, got_dv0, er):
+    """Against the all-fp64 oracle from the same fp32 inputs on the sampled
+    elements: p_K within FWD_RTOL of its summed scales, the final moments and
+    the meta-gradients norm-relative (the end-to-end bars of the parity tests)."""
+    K = hG.shape[0]
+    z = np.zeros(h_p0.size)
+    pK_ref, mt, vt = oracle.unrolled_fwd(h_p0, hG, z, z, 0, LR, B1, B2, EPS, er)
+    mag_p = np.abs(h_p0)
+    for k in range(K):
+        mag_p = mag_p + oracle.adam_fwd_mag(h_p0, hG[k], mt[k], vt[k], k, LR, B1, B2, EPS, er)[3]
+    assert_mag_close(got_pK, pK_ref, mag_p, FWD_RTOL, "p_K")
+    assert stats(got_muK, mt[K])[1] < FWD_RTOL and stats(got_nuK, vt[K])[1] < FWD_RTOL
+    _, dg_r, dm_r, dv_r = oracle.unrolled_bwd(h_cot, hG, mt, vt, 0, LR, B1, B2, EPS, er)
+    worst = max([stats(got_dg[k], dg_r[k])[1] for k in range(K)] + [stats(got_dm0, dm_r)[1],
+                                                                     stats(got_dv0, dv_r)[1]])
+    assert worst < BWD_RTOL, worst
+
+
+def test_recomputed_trajectory_past_2_31():
+    # flat K-step driver with nothing stored between the initial and final
+    # states: the VJP recomputes the moments (the benchmark's policy)
+    import paper_2211_06934_amd as P
+    n, K, er = BIG, 3, 1e-8
+    p0 = torch_normal(n, 0.05, 50, "cuda")
+    G = [torch_normal(n, 1e-3, 51 + k, "cuda") for k in range(K)]
+    mt = [torch.zeros(n, device="cuda")] + [None] * (K - 1) + [torch.empty(n, device="cuda")]
+    vt = [torch.zeros(n, device="cuda")] + [None] * (K - 1) + [torch.empty(n, device="cuda")]
+    pK = torch.empty(n, device="cuda")
+    P.adam_unrolled_fwd(p0, G, mt, vt, pK, 0, LR, B1, B2, EPS, er)
+    cot = torch_normal(n, 1.0, 55, "cuda")
+    dg = [torch.empty(n, device="cuda") for _ in range(K)]
+    dm0, dv0 = torch.empty(n, device="cuda"), torch.empty(n, device="cuda")
+    P.adam_unrolled_bwd(cot, G, mt, vt, dg, dm0, dv0, 0, LR, B1, B2, EPS, er)
+    torch.cuda.synchronize()
+    ti = torch.from_numpy(_index(n, 13)).cuda()
+    _end_to_end(_take(p0, ti), np.stack([_take(x, ti) for x in G]), _take(cot, ti), _take(pK, ti),
+                _take(mt[K], ti), _take(vt[K], ti), [_take(x, ti) for x in dg], _take(dm0, ti), _take(dv0, ti), er)
+
+
+def test_leaf_direct_recomputed_trajectory_past_2_31():
+    import paper_2211_06934_amd as P
+    numel = [3, (1 << 31) + 5]
+    table = P.segtable_create(numel)
+    K, er = 3, 0.0
+
+    def tree(std=None, seed=0, zero=False):
+        if zero:
+            return [torch.zeros(k, device="cuda") for k in numel]
+        if std is None:
+            return [torch.empty(k, device="cuda") for k in numel]
+        return [torch_normal(k, std, seed + j, "cuda") for j, k in enumerate(numel)]
+
+    ptr = lambda t: torch.tensor([x.data_ptr() for x in t], dtype=torch.int64, device="cuda")  # noqa: E731
+    p0 = tree(0.05, 60)
+    G = [tree(1e-3, 62 + 2 * k) for k in range(K)]
+    mu0, nu0, muK, nuK = tree(zero=True), tree(zero=True), tree(), tree()  # held: the VJP reads mu0, nu0
+    mu = [ptr(mu0)] + [None] * (K - 1) + [ptr(muK)]
+    nu = [ptr(nu0)] + [None] * (K - 1) + [ptr(nuK)]
+    pK = tree()
+    P.adam_unrolled_fwd_tree(table, ptr(p0), [ptr(t) for t in G], mu, nu, ptr(pK), 0, LR, B1, B2, EPS, er)
+    cot = tree(1.0, 70)
+    dg = [tree() for _ in range(K)]
+    dm0, dv0 = tree(), tree()
+    P.adam_unrolled_bwd_tree(table, ptr(cot), [ptr(t) for t in G], mu, nu, [ptr(t) for t in dg], ptr(dm0),
+                             ptr(dv0), 0, LR, B1, B2, EPS, er)
+    torch.cuda.synchronize()
+    ti = torch.from_numpy(_index(numel[1], 17)).cuda()
+    h = lambda t: _take(t[1], ti)  # noqa: E731
+    _end_to_end(h(p0), np.stack([h(t) for t in G]), h(cot), h(pK), h(muK), h(nuK), [h(t) for t in dg], h(dm0),
+                h(dv0), er)

@@ -157,6 +157,25 @@ def test_python_tree_api_roundtrip():
     assert back["a"][1]["y"] is None and isinstance(back["a"], tuple)
 
 
+@pytest.mark.parametrize("raw", [False, True])
+def test_python_tree_api_on_a_side_stream(raw):
+    # the copies run on the given stream (a torch stream or a raw hipStream_t
+    # address); the leaf-address arrays are allocated on that stream too
+    import paper_2211_06934_amd as P
+    torch.manual_seed(1)
+    tree = [torch.randn(k, device="cuda") for k in (5, 4096 + 3, 1, 70000)]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    s = side.cuda_stream if raw else side
+    flat = torch.empty(sum(x.numel() for x in tree), device="cuda")
+    flat, spec = P.tree.flatten(tree, out=flat, stream=s)
+    outs = [torch.empty_like(x) for x in tree]
+    back = P.tree.unflatten(flat, spec, out_leaves=outs, stream=s)
+    side.synchronize()
+    assert torch.equal(flat, torch.cat(tree))
+    assert all(torch.equal(a, b) for a, b in zip(back, tree))
+
+
 def test_many_small_full_size_bit_exact():
     # The 20,000-leaf workload at full size: flatten separately allocated leaves,
     # compare the whole flat buffer with the oracle's pack, then unflatten.
