@@ -111,11 +111,15 @@ def test_recomputed_trajectory_equals_stored_bitwise(K, n, count0, er, nz, polic
 
 @pytest.mark.parametrize("offset", [1, 4])
 @pytest.mark.parametrize("in_place", [False, True])
-def test_recomputed_misaligned_and_in_place(offset, in_place):
-    K, n = 6, 3 * 4096 + 5
+@pytest.mark.parametrize("K,policy", [(6, (2,)), (19, (4, 11, 18))])
+def test_recomputed_misaligned_and_in_place(offset, in_place, K, policy):
+    # K = 19: state 16 is not stored, so the running moments cross the
+    # forward's launch boundary through the final-state buffers (element
+    # kernels when offset is not a multiple of 4)
+    n = 3 * 4096 + 5
     inp = _inputs(K, n, 17, True)
     ref = _run(*inp, 0, 1e-8, "all")
-    got = _run(*inp, 0, 1e-8, (2,), in_place=in_place, offset=offset)
+    got = _run(*inp, 0, 1e-8, policy, in_place=in_place, offset=offset)
     torch.cuda.synchronize()
     _compare(got, ref, K)
 
@@ -144,7 +148,7 @@ def test_recomputed_run_against_oracle():
     assert worst < BWD_RTOL, worst
 
 
-@pytest.mark.parametrize("name", ["many_small", "resnet18_k10"])
+@pytest.mark.parametrize("name", ["many_small", "resnet18_k10", "convnet32", "tiny_mlp", "resnet18_k1"])
 def test_recomputed_full_size_equals_stored(name):
     # the benchmark's shapes and launch configuration: nothing stored between
     # the initial and final states (resnet18_k10: every 8th state)
