@@ -166,6 +166,33 @@ def test_recomputed_full_size_equals_stored(name):
     _compare(got, ref, K)
 
 
+def test_recomputed_zero_over_zero_points():
+    # fresh state, eps_root = 0 and exactly zero gradients: wherever v and g
+    # are both 0 a step meets the explicit 0/0 case (s = 0).  One quarter of
+    # the elements has g = 0 at every step, one quarter only at step 1.
+    K, n, er = 3, 4 * 4096 + 3, 0.0
+    p0, grads, m0, v0, cot = _inputs(K, n, 41, False)
+    q = n // 4
+    for k in range(K):
+        grads[k][:q] = 0.0
+    grads[0][q:2 * q] = 0.0
+    ref = _run(p0, grads, m0, v0, cot, 0, er, "all")
+    got = _run(p0, grads, m0, v0, cot, 0, er, "none")
+    torch.cuda.synchronize()
+    _compare(got, ref, K)
+    for t in [*got[3], got[4], got[5]]:
+        assert torch.isfinite(t).all()
+    # and against the fp64 oracle (same 0/0 reading), end to end
+    h = lambda t: t.cpu().numpy().astype(np.float64)  # noqa: E731
+    hg = np.stack([h(x) for x in grads])
+    z = np.zeros(n)
+    _, mt_ref, vt_ref = oracle.unrolled_fwd(h(p0), hg, z, z, 0, LR, B1, B2, EPS, er)
+    _, dg_r, dm0_r, dv0_r = oracle.unrolled_bwd(h(cot), hg, mt_ref, vt_ref, 0, LR, B1, B2, EPS, er)
+    worst = max([stats(h(got[3][k]), dg_r[k])[1] for k in range(K)] + [stats(h(got[4]), dm0_r)[1],
+                                                                        stats(h(got[5]), dv0_r)[1]])
+    assert worst < BWD_RTOL, worst
+
+
 def test_store_policies_the_backward_cannot_serve_are_rejected():
     import paper_2211_06934_amd as P
     K, n = 10, 64
