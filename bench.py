@@ -1,11 +1,11 @@
 """Benchmark of the differentiable-Adam hot path on one MI355X.
 
 One step = one pass of the whole path over one batch of synthetic input:
-  tree flatten of the params tree and of K gradient trees
+  tree flatten of the params tree and of K gradient trees (one batched launch)
   -> K-step unrolled Adam forward (the K steps fused in one kernel per 16
      steps, running params in registers, trajectory kept)
   -> K-step unrolled Adam backward (the same, running cotangents in registers)
-  -> tree unflatten of p_K and of the K gradient cotangents.
+  -> tree unflatten of p_K and of the K gradient cotangents (one batched launch).
 Default workload: the many-small-tensor tree (20,000 fp32 leaves, log-uniform
 sizes in [1, 65536], K = 3).  All inputs are resident in HBM before timing.
 Other trees (--workload tiny_mlp | convnet32 | resnet18_k1 | resnet18_k10)
@@ -46,6 +46,7 @@ TREE_UNROLL_CHUNK = 8  # the same for its leaf-direct form
 
 
 REMAT_SPAN = 8      # longest run of steps whose moments the backward recomputes
+COPY_BATCH = 16     # trees per launch of the batched flatten / unflatten
 
 
 def stored_states(K, trajectory):
@@ -201,9 +202,7 @@ def step_tree(P, S, ev=None):
     args = (S["count0"], h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
     if ev:
         ev[0].record()
-    P.tree_flatten(S["table"], S["p_ptrs"], S["p0"])
-    for k in range(S["K"]):
-        P.tree_flatten(S["table"], S["g_ptrs"][k], S["g"][k])
+    P.tree_flatten_batch(S["table"], [S["p_ptrs"]] + S["g_ptrs"], [S["p0"]] + S["g"])
     if ev:
         ev[1].record()
     P.adam_unrolled_fwd(S["p0"], S["g"], S["mu"], S["nu"], S["pK"], *args)
@@ -212,9 +211,7 @@ def step_tree(P, S, ev=None):
     P.adam_unrolled_bwd(S["cot"], S["g"], S["mu"], S["nu"], S["dg"], S["dm0"], S["dv0"], *args)
     if ev:
         ev[3].record()
-    P.tree_unflatten(S["table"], S["pK"], S["pK_ptrs"])
-    for k in range(S["K"]):
-        P.tree_unflatten(S["table"], S["dg"][k], S["dg_ptrs"][k])
+    P.tree_unflatten_batch(S["table"], [S["pK"]] + S["dg"], [S["pK_ptrs"]] + S["dg_ptrs"])
     if ev:
         ev[4].record()
 
@@ -224,11 +221,12 @@ def phases_tree(S):
     K, n = S["K"], S["n"]
     fl, fb = fwd_plan(K, S["stored"], UNROLL_CHUNK)
     bl, bb = bwd_plan(K, S["stored"], UNROLL_CHUNK)
+    cl = -(-(K + 1) // COPY_BATCH)  # the K + 1 trees go in batches of COPY_BATCH per launch
     return [
-        ("flatten", "tree_flatten", K + 1, (K + 1) * B_COPY * n),
+        ("flatten", "tree_flatten", cl, (K + 1) * B_COPY * n),
         ("adam_fwd", "adam_unrolled_fwd", fl, fb * n),
         ("adam_bwd", "adam_unrolled_bwd", bl, bb * n),
-        ("unflatten", "tree_unflatten", K + 1, (K + 1) * B_COPY * n),
+        ("unflatten", "tree_unflatten", cl, (K + 1) * B_COPY * n),
     ]
 
 

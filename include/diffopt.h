@@ -109,6 +109,22 @@ int diffopt_tree_flatten(const diffopt_segtable* table,
 int diffopt_tree_unflatten(const diffopt_segtable* table, const void* flat,
                            const uint64_t* leaf_ptrs, void* stream);
 
+/* Batched forms: ntrees trees of the same structure (one table) in one
+ * launch per 16 trees, e.g. the params tree and the K gradient trees of an
+ * unrolled inner loop (Listing 1 flattens each of them).  Tree t is
+ * leaf_ptrs[t] (a DEVICE array [nseg] of leaf addresses, as above) and
+ * flats[t] (its flat buffer); leaf_ptrs and flats are HOST arrays [ntrees].
+ * The result equals ntrees calls of diffopt_tree_flatten /
+ * diffopt_tree_unflatten; no tree may overlap another tree's buffers.
+ * ntrees == 0 is a no-op.                                                   */
+int diffopt_tree_flatten_batch(const diffopt_segtable* table, int64_t ntrees,
+                               const uint64_t* const* leaf_ptrs,
+                               void* const* flats, void* stream);
+
+int diffopt_tree_unflatten_batch(const diffopt_segtable* table, int64_t ntrees,
+                                 const void* const* flats,
+                                 const uint64_t* const* leaf_ptrs, void* stream);
+
 /* -------------------------------------------------------------------------
  * Differentiable Adam step, forward (Sec. 2.3; Listing 1's
  * opt.update(..., inplace=False) followed by apply_updates, fused).

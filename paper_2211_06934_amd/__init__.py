@@ -13,6 +13,7 @@ from .diffopt import (DiffoptError, SegTable, adam_bwd, adam_bwd_tree, adam_fwd,
                       adam_unrolled_bwd, adam_unrolled_bwd_tree, adam_unrolled_fwd,
                       adam_unrolled_fwd_tree, last_error, segtable_create, segtable_destroy,
                       segtable_nseg, segtable_total, tree_flatten, tree_unflatten,
+                      tree_flatten_batch, tree_unflatten_batch,
                       sgd_fwd, sgd_bwd, rmsprop_fwd, rmsprop_bwd, es_perturb, es_estimate)
 from . import tree
 from . import autograd
@@ -23,6 +24,7 @@ __all__ = [
     "adam_unrolled_bwd", "adam_unrolled_fwd", "adam_fwd_tree", "adam_bwd_tree",
     "adam_unrolled_fwd_tree", "adam_unrolled_bwd_tree", "sgd_fwd", "sgd_bwd", "rmsprop_fwd", "rmsprop_bwd",
     "es_perturb", "es_estimate", "last_error", "segtable_create", "segtable_destroy",
-    "segtable_nseg", "segtable_total", "tree_flatten", "tree_unflatten", "AdamFn", "AdamHyper",
+    "segtable_nseg", "segtable_total", "tree_flatten", "tree_unflatten", "tree_flatten_batch",
+    "tree_unflatten_batch", "AdamFn", "AdamHyper",
     "AdamState", "FlatAdam", "AdamTreeFn", "MetaAdam",
 ]

@@ -592,7 +592,7 @@ void launch_urbwd(bool vec, const URBwdArgs& a, hipStream_t st) {
 }
 
 // Run length C is a template argument so the trajectory stays in registers.
-void launch_urbwd_c(int C, bool vec, const URBwdArgs& a, hipStream_t st) {
+int launch_urbwd_c(const char* who, int C, bool vec, const URBwdArgs& a, hipStream_t st) {
   switch (C) {
     case 1: launch_urbwd<1>(vec, a, st); break;
     case 2: launch_urbwd<2>(vec, a, st); break;
@@ -601,8 +601,10 @@ void launch_urbwd_c(int C, bool vec, const URBwdArgs& a, hipStream_t st) {
     case 5: launch_urbwd<5>(vec, a, st); break;
     case 6: launch_urbwd<6>(vec, a, st); break;
     case 7: launch_urbwd<7>(vec, a, st); break;
-    default: launch_urbwd<8>(vec, a, st); break;
+    case 8: launch_urbwd<8>(vec, a, st); break;
+    default: return fail(DIFFOPT_EINVAL, "%s: recompute run of %d steps (at most %d)", who, C, kRS);
   }
+  return DIFFOPT_OK;
 }
 static_assert(kRS == 8, "launch_urbwd_c instantiates run lengths 1..8");
 
@@ -849,7 +851,8 @@ extern "C" int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
         if (on) make_coef(who, count0 + j + s, lr, b1, b2, eps, eps_root, &a.c[s]);
         else a.c[s] = AdamCoef{};
       }
-      launch_urbwd_c(C, vec, a, st);
+      rc = launch_urbwd_c(who, C, vec, a, st);
+      if (rc) return rc;
       khi = j;
     }
     rc = launch_status(who);

@@ -92,11 +92,19 @@ __device__ __forceinline__ u32x4 funnel(u32x4 w0, u32x4 w1, uint32_t s) {
   }
 }
 
+// Trees of one structure copied by one launch: grid y selects the tree.
+constexpr int kMaxBatch = 16;
+struct CopyBatch {
+  const uint64_t* leaf_ptrs[kMaxBatch];  // device arrays of leaf addresses
+  uint64_t flat[kMaxBatch];              // flat buffers
+};
+
 template <int E, bool PACK>
 __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restrict__ seg,
                                                         const int64_t* __restrict__ tile_first, int64_t ngroups,
-                                                        const uint64_t* __restrict__ leaf_ptrs, uint64_t flat,
-                                                        int dense_orig) {
+                                                        CopyBatch batch, int dense_orig) {
+  const uint64_t* __restrict__ leaf_ptrs = batch.leaf_ptrs[blockIdx.y];
+  const uint64_t flat = batch.flat[blockIdx.y];
   __shared__ int64_t s_goff[kWindowMax + 1];
   __shared__ int64_t s_fbase[kWindowMax];  // flat byte address of the leaf's range
   __shared__ int64_t s_bytes[kWindowMax];
@@ -289,48 +297,83 @@ extern "C" int64_t diffopt_segtable_nseg(const diffopt_segtable* t) { return t ?
 
 namespace {
 
+// ntrees copies of one structure: leaf_ptrs[t] is tree t's device array of
+// leaf addresses, flat[t] its flat buffer; up to kMaxBatch trees per launch.
 template <bool PACK>
-int tree_copy(const char* who, const diffopt_segtable* t, const uint64_t* leaf_ptrs, uint64_t flat, void* stream) {
+int tree_copy(const char* who, const diffopt_segtable* t, int64_t ntrees, const uint64_t* const* leaf_ptrs,
+              const uint64_t* flat, void* stream) {
   if (!t) return fail(DIFFOPT_EINVAL, "%s: table is NULL", who);
-  if (t->ntiles == 0) return DIFFOPT_OK;
-  if (!leaf_ptrs || !flat) return fail(DIFFOPT_EINVAL, "%s: null leaf_ptrs or flat", who);
-  if (flat % (uint64_t)t->elem_bytes != 0)
-    return fail(DIFFOPT_EINVAL, "%s: flat is not aligned to elem_bytes", who);
+  if (ntrees < 0) return fail(DIFFOPT_EINVAL, "%s: ntrees must be >= 0", who);
+  if (t->ntiles == 0 || ntrees == 0) return DIFFOPT_OK;
+  for (int64_t k = 0; k < ntrees; ++k) {
+    if (!leaf_ptrs[k] || !flat[k]) return fail(DIFFOPT_EINVAL, "%s: null leaf_ptrs or flat (tree %lld)", who,
+                                               (long long)k);
+    if (flat[k] % (uint64_t)t->elem_bytes != 0)
+      return fail(DIFFOPT_EINVAL, "%s: flat buffer of tree %lld is not aligned to elem_bytes", who, (long long)k);
+  }
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != t->device)
     return fail(DIFFOPT_EINVAL, "%s: the table lives on device %d, the current device is %d", who, t->device, dev);
   hipStream_t st = as_stream(stream);
-  dim3 grid((unsigned)t->ntiles), block(kTB);
-  switch (t->elem_bytes) {
-    case 1:
-      hipLaunchKernelGGL((tree_copy_kernel<1, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                         leaf_ptrs, flat, t->dense_orig);
-      break;
-    case 2:
-      hipLaunchKernelGGL((tree_copy_kernel<2, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                         leaf_ptrs, flat, t->dense_orig);
-      break;
-    case 4:
-      hipLaunchKernelGGL((tree_copy_kernel<4, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                         leaf_ptrs, flat, t->dense_orig);
-      break;
-    default:
-      hipLaunchKernelGGL((tree_copy_kernel<8, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                         leaf_ptrs, flat, t->dense_orig);
-      break;
+  for (int64_t k0 = 0; k0 < ntrees; k0 += kMaxBatch) {
+    const int nb = (int)(ntrees - k0 < kMaxBatch ? ntrees - k0 : kMaxBatch);
+    CopyBatch batch{};
+    for (int k = 0; k < nb; ++k) {
+      batch.leaf_ptrs[k] = leaf_ptrs[k0 + k];
+      batch.flat[k] = flat[k0 + k];
+    }
+    dim3 grid((unsigned)t->ntiles, (unsigned)nb), block(kTB);
+    switch (t->elem_bytes) {
+      case 1:
+        hipLaunchKernelGGL((tree_copy_kernel<1, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
+                           batch, t->dense_orig);
+        break;
+      case 2:
+        hipLaunchKernelGGL((tree_copy_kernel<2, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
+                           batch, t->dense_orig);
+        break;
+      case 4:
+        hipLaunchKernelGGL((tree_copy_kernel<4, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
+                           batch, t->dense_orig);
+        break;
+      default:
+        hipLaunchKernelGGL((tree_copy_kernel<8, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
+                           batch, t->dense_orig);
+        break;
+    }
+    int rc = launch_status(who);
+    if (rc) return rc;
   }
-  return launch_status(who);
+  return DIFFOPT_OK;
 }
 
 }  // namespace
 
 extern "C" int diffopt_tree_flatten(const diffopt_segtable* t, const uint64_t* leaf_ptrs, void* flat, void* stream) {
   clear_error();
-  return tree_copy<true>("diffopt_tree_flatten", t, leaf_ptrs, reinterpret_cast<uint64_t>(flat), stream);
+  const uint64_t f = reinterpret_cast<uint64_t>(flat);
+  return tree_copy<true>("diffopt_tree_flatten", t, 1, &leaf_ptrs, &f, stream);
 }
 
 extern "C" int diffopt_tree_unflatten(const diffopt_segtable* t, const void* flat, const uint64_t* leaf_ptrs,
                                       void* stream) {
   clear_error();
-  return tree_copy<false>("diffopt_tree_unflatten", t, leaf_ptrs, reinterpret_cast<uint64_t>(flat), stream);
+  const uint64_t f = reinterpret_cast<uint64_t>(flat);
+  return tree_copy<false>("diffopt_tree_unflatten", t, 1, &leaf_ptrs, &f, stream);
+}
+
+extern "C" int diffopt_tree_flatten_batch(const diffopt_segtable* t, int64_t ntrees, const uint64_t* const* leaf_ptrs,
+                                          void* const* flats, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_tree_flatten_batch";
+  if (ntrees > 0 && (!leaf_ptrs || !flats)) return fail(DIFFOPT_EINVAL, "%s: null pointer array", who);
+  return tree_copy<true>(who, t, ntrees, leaf_ptrs, reinterpret_cast<const uint64_t*>(flats), stream);
+}
+
+extern "C" int diffopt_tree_unflatten_batch(const diffopt_segtable* t, int64_t ntrees, const void* const* flats,
+                                            const uint64_t* const* leaf_ptrs, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_tree_unflatten_batch";
+  if (ntrees > 0 && (!leaf_ptrs || !flats)) return fail(DIFFOPT_EINVAL, "%s: null pointer array", who);
+  return tree_copy<false>(who, t, ntrees, leaf_ptrs, reinterpret_cast<const uint64_t*>(flats), stream);
 }

@@ -576,7 +576,7 @@ void launch_trbwd(const diffopt_segtable* t, const TRBwdArgs& a, hipStream_t st)
 }
 
 // Run length C is a template argument so the trajectory stays in registers.
-void launch_trbwd_c(int C, const diffopt_segtable* t, const TRBwdArgs& a, hipStream_t st) {
+int launch_trbwd_c(const char* who, int C, const diffopt_segtable* t, const TRBwdArgs& a, hipStream_t st) {
   switch (C) {
     case 1: launch_trbwd<1>(t, a, st); break;
     case 2: launch_trbwd<2>(t, a, st); break;
@@ -585,8 +585,10 @@ void launch_trbwd_c(int C, const diffopt_segtable* t, const TRBwdArgs& a, hipStr
     case 5: launch_trbwd<5>(t, a, st); break;
     case 6: launch_trbwd<6>(t, a, st); break;
     case 7: launch_trbwd<7>(t, a, st); break;
-    default: launch_trbwd<8>(t, a, st); break;
+    case 8: launch_trbwd<8>(t, a, st); break;
+    default: return fail(DIFFOPT_EINVAL, "%s: recompute run of %d steps (at most %d)", who, C, kTRS);
   }
+  return DIFFOPT_OK;
 }
 static_assert(kTRS == 8, "launch_trbwd_c instantiates run lengths 1..8");
 
@@ -779,7 +781,8 @@ extern "C" int diffopt_adam_unrolled_bwd_tree(const diffopt_segtable* table, int
         a.a[6 + 2 * s] = dgrads[j + s];
         make_coef(who, count0 + j + s, lr, b1, b2, eps, eps_root, &a.c[s]);
       }
-      launch_trbwd_c(C, table, a, st);
+      rc = launch_trbwd_c(who, C, table, a, st);
+      if (rc) return rc;
       khi = j;
     }
     rc = launch_status(who);

@@ -46,6 +46,8 @@ def _load_library():
         "diffopt_segtable_nseg": (i64, [vp]),
         "diffopt_tree_flatten": (ctypes.c_int, [vp, vp, vp, vp]),
         "diffopt_tree_unflatten": (ctypes.c_int, [vp, vp, vp, vp]),
+        "diffopt_tree_flatten_batch": (ctypes.c_int, [vp, i64, pp, pp, vp]),
+        "diffopt_tree_unflatten_batch": (ctypes.c_int, [vp, i64, pp, pp, vp]),
         "diffopt_adam_fwd": (ctypes.c_int, [vp, vp, vp, vp, i64, *hyper, vp, vp, vp, vp, vp]),
         "diffopt_adam_bwd": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, i64, *hyper, vp, vp, vp, vp, vp]),
         "diffopt_adam_unrolled_fwd": (ctypes.c_int, [i64, i64, vp, pp, pp, pp, vp, *hyper, vp]),
@@ -185,6 +187,31 @@ def tree_unflatten(table: SegTable, flat, leaf_ptrs, stream=None) -> None:
     """diffopt_tree_unflatten."""
     _check(_lib.diffopt_tree_unflatten(table.handle, _addr(flat, "flat", None),
                                        _addr(leaf_ptrs, "leaf_ptrs", torch.int64), _stream(stream)))
+
+
+def _raw_array(items, what, conv):
+    arr = (ctypes.c_void_p * max(len(items), 1))()
+    for i, t in enumerate(items):
+        arr[i] = conv(t, "%s[%d]" % (what, i))
+    return arr
+
+
+def tree_flatten_batch(table: SegTable, leaf_ptrs: Sequence, flats: Sequence, stream=None) -> None:
+    """diffopt_tree_flatten_batch: tree t is (leaf_ptrs[t], flats[t])."""
+    if len(leaf_ptrs) != len(flats):
+        raise ValueError("leaf_ptrs and flats need one entry per tree")
+    _check(_lib.diffopt_tree_flatten_batch(
+        table.handle, len(flats), _raw_array(leaf_ptrs, "leaf_ptrs", lambda t, w: _addr(t, w, torch.int64)),
+        _raw_array(flats, "flats", lambda t, w: _addr(t, w, None)), _stream(stream)))
+
+
+def tree_unflatten_batch(table: SegTable, flats: Sequence, leaf_ptrs: Sequence, stream=None) -> None:
+    """diffopt_tree_unflatten_batch."""
+    if len(leaf_ptrs) != len(flats):
+        raise ValueError("leaf_ptrs and flats need one entry per tree")
+    _check(_lib.diffopt_tree_unflatten_batch(
+        table.handle, len(flats), _raw_array(flats, "flats", lambda t, w: _addr(t, w, None)),
+        _raw_array(leaf_ptrs, "leaf_ptrs", lambda t, w: _addr(t, w, torch.int64)), _stream(stream)))
 
 
 def adam_fwd(params, grad, mu, nu, count, lr, b1, b2, eps, eps_root,

@@ -200,3 +200,44 @@ def test_many_small_full_size_bit_exact():
     torch.cuda.synchronize()
     got = torch.cat(outs).cpu().numpy()
     assert_bits_equal(got, np.concatenate(host_leaves), "unflatten 20k")
+
+
+@pytest.mark.parametrize("eb", [4, 1, 8])
+@pytest.mark.parametrize("ntrees", [1, 3, 16, 17, 40])
+def test_batched_copies_bit_exact(eb, ntrees):
+    # ntrees trees of one structure in one call (one launch per 16 trees):
+    # every tree's flat buffer equals the oracle's pack of its leaves, and
+    # the batched unflatten rebuilds every tree, bit for bit; gaps between
+    # leaves (explicit offsets) keep the flat buffer's bits
+    import paper_2211_06934_amd as P
+    ndt, tdt = DT[eb]
+    rng = np.random.default_rng(eb * 100 + ntrees)
+    numel = [0, 3] + [int(k) for k in rng.integers(0, 2500, size=60)] + [0, 4096 + 1]
+    offsets, pos = [], 0
+    for k in numel:
+        pos += int(rng.integers(0, 5))
+        offsets.append(pos)
+        pos += k
+    table = P.segtable_create(numel, offsets, eb)
+    n = table.total
+    host = [[random_bits(k, ndt, seed=1000 * t + j) for j, k in enumerate(numel)] for t in range(ntrees)]
+    trees = [_make_leaves(h, tdt, "packed-views" if t % 2 else "separate", seed=t) for t, h in enumerate(host)]
+    fills = [random_bits(max(n, 1), ndt, seed=77 + t)[:n] for t in range(ntrees)]
+    flats = [_np_to_dev(f, tdt) for f in fills]
+    P.tree_flatten_batch(table, [_ptrs(x) for x in trees], flats)
+    outs = [_make_leaves([np.zeros(k, ndt) for k in numel], tdt, "separate", seed=50 + t) for t in range(ntrees)]
+    P.tree_unflatten_batch(table, flats, [_ptrs(x) for x in outs])
+    torch.cuda.synchronize()
+    for t in range(ntrees):
+        expect = np.array(fills[t], copy=True)
+        packed = oracle.pack(host[t], flat_len=n, offsets=offsets, dtype=ndt)
+        for o, k in zip(offsets, numel):
+            expect[o:o + k] = packed[o:o + k]
+        assert_bits_equal(flats[t].cpu().numpy().view(ndt), expect, "flatten tree %d" % t)
+        for j, (o, r) in enumerate(zip(outs[t], host[t])):
+            assert_bits_equal(o.cpu().numpy().view(ndt), r, "unflatten tree %d leaf %d" % (t, j))
+    # no trees is a no-op; mismatched lists are refused before any launch
+    P.tree_flatten_batch(table, [], [])
+    with pytest.raises(ValueError):
+        P.tree_unflatten_batch(table, flats[:1], [])
+    table.close()
