@@ -4,7 +4,7 @@ single-step kernels, in the same order, so the fused driver must reproduce the
 step-by-step composition of diffopt_adam_fwd / diffopt_adam_bwd bit for bit:
 at launch-chunk boundaries (K = 16, 17, 33), ragged lengths (the n % 4 tail
 elements), nonzero initial moments, in-place p_K == p0, and misaligned buffers
-(which take the step-by-step path inside the driver).  One K = 20 run is also
+(which take the one-element-per-lane fused kernels).  One K = 20 run is also
 checked against the oracle directly."""
 import numpy as np
 import pytest
