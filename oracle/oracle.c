@@ -46,7 +46,9 @@
  *   backward: step-1 closed form; linearity in the cotangents; autograd
  *             through torch.optim's functional Adam (differentiable mode) in
  *             fp64; fp64 central differences of the forward, including the
- *             symmetric difference at g = 0 (reading R3).
+ *             symmetric difference at g = 0 (reading R3) and, from a fresh
+ *             state (m = 0), the one-sided difference in v there, which is
+ *             exactly 0 since the update vanishes for every v >= 0.
  *   unrolled: fp64 central differences of the K-step map.
  *   pack    : numpy concatenation, bit for bit; unpack(pack(x)) == x.
  *   mag_*   : the tolerance scales are sums of absolute values of terms and

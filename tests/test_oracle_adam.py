@@ -255,6 +255,15 @@ def test_zero_over_zero_is_symmetric_derivative():
         fd = dP * (up - um) / (2 * h)
         assert _rel(dg, fd) < tol, count
         assert np.all(dv == 0.0)
+    # The nu-cotangent there.  From a fresh state (m = 0, the case the inner
+    # loop reaches), m' = 0, so the update is 0 for every v >= 0 and the exact
+    # derivative in v is 0: the one-sided difference quotient pins the value.
+    # With m != 0 the one-sided slope is unbounded, and 0 is a convention.
+    _, _, _, dv = oracle.adam_bwd(dP, None, None, z, z, z, 0, LR, B1, B2, EPS, 0.0)
+    for h in (1e-30, 1e-12, 1e-4):
+        u1 = oracle.adam_fwd(z, z, z, z + h, 0, LR, B1, B2, EPS, 0.0)[0]
+        u0 = oracle.adam_fwd(z, z, z, z, 0, LR, B1, B2, EPS, 0.0)[0]
+        assert np.array_equal(dv, dP * (u1 - u0) / h)
 
 
 def test_mag_bounds_values():
