@@ -51,10 +51,13 @@ COPY_BATCH = 16     # trees per launch of the batched flatten / unflatten
 
 def stored_states(K, trajectory):
     """Indices 1..K of the moment states the forward stores: all of them, or
-    (recompute) only the final one and every REMAT_SPAN-th."""
+    (recompute) the final one and as few others as the backward needs, evenly
+    spaced so its recompute runs are as short as possible (K = 10: state 5,
+    two runs of 5 steps; the bytes equal those of storing state 8)."""
     if trajectory == "stored":
         return set(range(1, K + 1))
-    return set(range(REMAT_SPAN, K, REMAT_SPAN)) | {K}
+    runs = -(-K // REMAT_SPAN)
+    return {(K * r) // runs for r in range(1, runs)} | {K}
 
 
 def fwd_plan(K, stored, chunk):
@@ -596,8 +599,9 @@ def main():
                                 a.workload,
                                 "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg"),
                    "launch": "hip graph replay" if a.graph else "eager", "parallelism": "single GPU",
-                   **({"trajectory": {"recompute": "final moment state stored (and every %d-th); the VJP recomputes "
-                                                   "the rest" % REMAT_SPAN,
+                   **({"trajectory": {"recompute": "final moment state stored (and, for K > %d, evenly spaced ones "
+                                                   "so that no recompute run exceeds %d steps); the VJP recomputes "
+                                                   "the rest" % (REMAT_SPAN, REMAT_SPAN),
                                       "stored": "every moment state stored"}[a.trajectory]}
                       if "stored" in S else {})},
         "us_per_step": round(ms_step * 1e3, 2),

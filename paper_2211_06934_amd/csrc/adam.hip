@@ -41,6 +41,16 @@
 #ifndef DIFFOPT_URBWD_BLOCK
 #define DIFFOPT_URBWD_BLOCK 512  // threads per workgroup, fused VJP recomputing the moments
 #endif
+// Runs of at least DIFFOPT_URBWD_LONG_RUN steps use DIFFOPT_URBWD_BLOCK_LONG
+// threads.  Measured (n = 1.17e8): 512 threads are fastest for runs of 3 to 6
+// steps (256: 1-5% slower); an 8-step run (151 VGPRs) took 2.02 ms at 512 and
+// 1.91 ms at 256.
+#ifndef DIFFOPT_URBWD_LONG_RUN
+#define DIFFOPT_URBWD_LONG_RUN 7
+#endif
+#ifndef DIFFOPT_URBWD_BLOCK_LONG
+#define DIFFOPT_URBWD_BLOCK_LONG 256
+#endif
 
 namespace diffopt {
 
@@ -561,12 +571,12 @@ __device__ __forceinline__ void urbwd_element(int64_t e, const URBwdArgs& a) {
   a.dv[e] = dV;
 }
 
-template <int C>
-__global__ __launch_bounds__(kURB) void adam_unrolled_bwd_remat_vec(URBwdArgs a) {
+template <int C, int B>
+__global__ __launch_bounds__(B) void adam_unrolled_bwd_remat_vec(URBwdArgs a) {
   const int64_t nv = a.n >> 2;
-  const int64_t ntiles = (nv + kURB - 1) / kURB;
+  const int64_t ntiles = (nv + B - 1) / B;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t i = t * kURB + threadIdx.x;
+    const int64_t i = t * B + threadIdx.x;
     if (i < nv) urbwd_vector<C>(i, a);
   }
   if (blockIdx.x == gridDim.x - 1) {
@@ -575,20 +585,23 @@ __global__ __launch_bounds__(kURB) void adam_unrolled_bwd_remat_vec(URBwdArgs a)
   }
 }
 
-template <int C>
-__global__ __launch_bounds__(kURB) void adam_unrolled_bwd_remat_elem(URBwdArgs a) {
-  for (int64_t e = (int64_t)blockIdx.x * kURB + threadIdx.x; e < a.n; e += (int64_t)gridDim.x * kURB)
+template <int C, int B>
+__global__ __launch_bounds__(B) void adam_unrolled_bwd_remat_elem(URBwdArgs a) {
+  for (int64_t e = (int64_t)blockIdx.x * B + threadIdx.x; e < a.n; e += (int64_t)gridDim.x * B)
     urbwd_element<C>(e, a);
 }
 
+// Long runs hold more registers per lane, so fewer waves fit on a SIMD; they
+// take smaller workgroups so that whole workgroups still fill the CU.
 template <int C>
 void launch_urbwd(bool vec, const URBwdArgs& a, hipStream_t st) {
+  constexpr int B = C >= DIFFOPT_URBWD_LONG_RUN ? DIFFOPT_URBWD_BLOCK_LONG : kURB;
   if (vec)
-    hipLaunchKernelGGL((adam_unrolled_bwd_remat_vec<C>), dim3((unsigned)grid_for(((a.n >> 2) + kURB - 1) / kURB)),
-                       dim3(kURB), 0, st, a);
+    hipLaunchKernelGGL((adam_unrolled_bwd_remat_vec<C, B>), dim3((unsigned)grid_for(((a.n >> 2) + B - 1) / B)),
+                       dim3(B), 0, st, a);
   else
-    hipLaunchKernelGGL((adam_unrolled_bwd_remat_elem<C>), dim3((unsigned)grid_for((a.n + kURB - 1) / kURB)),
-                       dim3(kURB), 0, st, a);
+    hipLaunchKernelGGL((adam_unrolled_bwd_remat_elem<C, B>), dim3((unsigned)grid_for((a.n + B - 1) / B)), dim3(B),
+                       0, st, a);
 }
 
 // Run length C is a template argument so the trajectory stays in registers.

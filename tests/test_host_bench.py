@@ -37,13 +37,17 @@ def test_recomputed_trajectory_one_launch():
 
 def test_launch_boundaries():
     b = _bench()
-    # K = 10, recompute: state 8 stored as well.  Forward: one launch, two
-    # states out.  VJP: run (8, 10] reads state 8 (no running dM, dV in), run
-    # (0, 8] reads state 0 and the running dM, dV.
+    # K = 10, recompute: state 5 stored as well (two runs of 5 steps).
+    # Forward: one launch, two states out.  VJP: run (5, 10] reads state 5
+    # (no running dM, dV in), run (0, 5] reads state 0 and the running dM, dV.
     st = b.stored_states(10, "recompute")
-    assert st == {8, 10}
+    assert st == {5, 10}
     assert b.fwd_plan(10, st, 16) == (1, 16 + 40 + 16)
-    assert b.bwd_plan(10, st, 16) == (2, (4 + 8 + 8 + 2 * 8) + (4 + 8 + 8 + 8 + 8 * 8))
+    assert b.bwd_plan(10, st, 16) == (2, (4 + 8 + 8 + 5 * 8) + (4 + 8 + 8 + 8 + 5 * 8))
+    # the same bytes as storing state 8 (runs of 2 and 8)
+    assert b.bwd_plan(10, {8, 10}, 16)[1] == b.bwd_plan(10, st, 16)[1]
+    assert b.stored_states(17, "recompute") == {5, 11, 17}  # runs of 5, 6, 6
+    assert b.stored_states(16, "recompute") == {8, 16}
     # K = 17, whole trajectory: two forward launches (16 + 1 steps), p, mu, nu
     # re-read and p re-written at the boundary; two VJP launches, the second
     # reading the running dM, dV.
