@@ -357,6 +357,42 @@ int diffopt_rmsprop_bwd(const float* dparams_out, const float* dnu_out,
                         float* dgrad, float* dnu_in, float* dmom_in,
                         void* stream);
 
+/* Leaf-direct ("tree map") forms of the four calls above (Appendix D,
+ * Table 2 "Tree Map"): the same arithmetic applied to every leaf of
+ * parameter trees, one launch each, with the conventions of the leaf-direct
+ * Adam calls (a table with elem_bytes == 4 on the current device; every other
+ * pointer a DEVICE array [nseg] of fp32 leaf addresses in table order, NULL
+ * where the flat call takes NULL; an output leaf may be its own input leaf).
+ * The result equals flatten -> flat call -> unflatten element for element. */
+int diffopt_sgd_fwd_tree(const diffopt_segtable* table, const uint64_t* params,
+                         const uint64_t* grad, const uint64_t* trace,
+                         double lr, double momentum, int32_t nesterov,
+                         const uint64_t* params_out, const uint64_t* trace_out,
+                         void* stream);
+
+int diffopt_sgd_bwd_tree(const diffopt_segtable* table,
+                         const uint64_t* dparams_out, const uint64_t* dtrace_out,
+                         double lr, double momentum, int32_t nesterov,
+                         const uint64_t* dgrad, const uint64_t* dtrace_in,
+                         void* stream);
+
+int diffopt_rmsprop_fwd_tree(const diffopt_segtable* table,
+                             const uint64_t* params, const uint64_t* grad,
+                             const uint64_t* nu, const uint64_t* mom,
+                             double lr, double alpha, double eps,
+                             double eps_root, double momentum,
+                             const uint64_t* params_out, const uint64_t* nu_out,
+                             const uint64_t* mom_out, void* stream);
+
+int diffopt_rmsprop_bwd_tree(const diffopt_segtable* table,
+                             const uint64_t* dparams_out,
+                             const uint64_t* dnu_out, const uint64_t* dmom_out,
+                             const uint64_t* grad, const uint64_t* nu,
+                             double lr, double alpha, double eps,
+                             double eps_root, double momentum,
+                             const uint64_t* dgrad, const uint64_t* dnu_in,
+                             const uint64_t* dmom_in, void* stream);
+
 /* -------------------------------------------------------------------------
  * Zero-order (evolution-strategies) gradient estimation (Sec. 2.2
  * "Zero-order Differentiation"): grad f_s(theta) = (1/s) E_z[f(theta + s z) z]

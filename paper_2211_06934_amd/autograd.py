@@ -1,4 +1,4 @@
-"""torch.autograd.Function around the fused differentiable Adam step.
+"""torch.autograd.Functions around the fused differentiable optimizer steps.
 
 Mirrors Listing 1's functional API: ``opt.init`` creates (mu, nu, count);
 ``opt.update(grads, state, inplace=False)`` followed by ``apply_updates`` is
@@ -125,27 +125,18 @@ class AdamTreeFn(torch.autograd.Function):
         return (None, None, None, *dP, *dg, *dm, *dv)
 
 
-class MetaAdam:
-    """Object-oriented differentiable Adam over a module's parameters
-    (Listing 1, OOP API: ``opt = MetaAdam(model); opt.step(loss)``).
+class _MetaOptimizer:
+    """Module-parameter plumbing shared by the object-oriented optimizers
+    (Listing 1, OOP API): the trainable parameters in registration order, one
+    cached segment table for their shapes, and the installation of updated,
+    non-leaf tensors as the module's parameters."""
 
-    Each step differentiates the loss w.r.t. the current parameters with
-    create_graph=True, applies one leaf-direct fused Adam step (AdamTreeFn) and
-    installs the updated, non-leaf tensors as the module's parameters, so a
-    later outer loss backpropagates through every inner step (explicit
-    gradient).  ``detach_()`` cuts the graph, e.g. between outer iterations.
-    """
-
-    def __init__(self, module: torch.nn.Module, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, eps_root=0.0):
+    def __init__(self, module: torch.nn.Module):
         from .tree import segment_table
         self.module = module
-        self.hyper = AdamHyper(lr, b1, b2, eps, eps_root)
         self.names = [n for n, p in module.named_parameters() if p.requires_grad]
         params = [self._get(n) for n in self.names]
         self.table = segment_table([tuple(p.shape) for p in params], params[0].dtype, params[0].device)
-        self.mu = [torch.zeros_like(p) for p in params]
-        self.nu = [torch.zeros_like(p) for p in params]
-        self.count = 0
 
     def _owner(self, name):
         mod = self.module
@@ -165,22 +156,226 @@ class MetaAdam:
     def params(self):
         return [self._get(n) for n in self.names]
 
+    def _install(self, new_params) -> None:
+        for name, p in zip(self.names, new_params):
+            self._set(name, p)
+
+    def _detach_params(self) -> None:
+        for name in self.names:
+            p = self._get(name)
+            self._set(name, torch.nn.Parameter(p.detach().clone()) if not isinstance(p, torch.nn.Parameter) else p)
+
+
+class MetaAdam(_MetaOptimizer):
+    """Object-oriented differentiable Adam over a module's parameters
+    (Listing 1, OOP API: ``opt = MetaAdam(model); opt.step(loss)``).
+
+    Each step differentiates the loss w.r.t. the current parameters with
+    create_graph=True, applies one leaf-direct fused Adam step (AdamTreeFn) and
+    installs the updated, non-leaf tensors as the module's parameters, so a
+    later outer loss backpropagates through every inner step (explicit
+    gradient).  ``detach_()`` cuts the graph, e.g. between outer iterations.
+    """
+
+    def __init__(self, module: torch.nn.Module, lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, eps_root=0.0):
+        super().__init__(module)
+        self.hyper = AdamHyper(lr, b1, b2, eps, eps_root)
+        params = self.params()
+        self.mu = [torch.zeros_like(p) for p in params]
+        self.nu = [torch.zeros_like(p) for p in params]
+        self.count = 0
+
     def step(self, loss: torch.Tensor) -> None:
         params = self.params()
         grads = torch.autograd.grad(loss, params, create_graph=True)
         out = AdamTreeFn.apply(self.table, self.count, self.hyper, *params, *grads, *self.mu, *self.nu)
         S = len(params)
-        for name, p in zip(self.names, out[:S]):
-            self._set(name, p)
+        self._install(out[:S])
         self.mu, self.nu = list(out[S:2 * S]), list(out[2 * S:])
         self.count += 1
 
     def detach_(self) -> None:
-        for name in self.names:
-            p = self._get(name)
-            self._set(name, torch.nn.Parameter(p.detach().clone()) if not isinstance(p, torch.nn.Parameter) else p)
+        self._detach_params()
         self.mu = [m.detach() for m in self.mu]
         self.nu = [v.detach() for v in self.nu]
+
+
+# ---- SGD-momentum and RMSProp (the paper's other fused optimizers) ------------------
+
+
+@dataclasses.dataclass(frozen=True)
+class SGDHyper:
+    lr: float = 0.1
+    momentum: float = 0.0
+    nesterov: bool = False
+
+
+@dataclasses.dataclass(frozen=True)
+class RMSPropHyper:
+    lr: float = 1e-2
+    alpha: float = 0.99
+    eps: float = 1e-8
+    eps_root: float = 0.0
+    momentum: float = 0.0
+
+
+def _ptrs_or_none(leaves, dev):
+    from .tree import leaf_pointer_tensor
+    return None if leaves is None else leaf_pointer_tensor(leaves, dev)
+
+
+class SGDTreeFn(torch.autograd.Function):
+    """Leaf-direct differentiable SGD step (momentum, Nesterov optional).
+
+    apply(table, hyper, has_trace, *leaves) with leaves = p_1..p_S, g_1..g_S
+    and, when has_trace, the trace t_1..t_S; returns p'_1..p'_S and, when
+    momentum > 0, t'_1..t'_S.  The VJP is linear in the cotangents, so nothing
+    is saved; absent cotangents go to the kernel as NULL (zero)."""
+
+    @staticmethod
+    def forward(ctx, table, hyper: SGDHyper, has_trace: bool, *leaves):
+        S = len(table.numel)
+        p, g = [x.contiguous() for x in leaves[:S]], [x.contiguous() for x in leaves[S:2 * S]]
+        t = [x.contiguous() for x in leaves[2 * S:3 * S]] if has_trace else None
+        mom = hyper.momentum > 0
+        dev = p[0].device
+        po = [torch.empty_like(x) for x in p]
+        to = [torch.empty_like(x) for x in p] if mom else None
+        _d.sgd_fwd_tree(table, _ptrs_or_none(p, dev), _ptrs_or_none(g, dev), _ptrs_or_none(t, dev), hyper.lr,
+                        hyper.momentum, hyper.nesterov, _ptrs_or_none(po, dev), _ptrs_or_none(to, dev))
+        ctx.table, ctx.hyper, ctx.has_trace, ctx.S = table, hyper, has_trace, S
+        ctx.shapes, ctx.dtype, ctx.device = [x.shape for x in p], p[0].dtype, dev
+        return (*po, *to) if mom else tuple(po)
+
+    @staticmethod
+    def backward(ctx, *cots):
+        S, h = ctx.S, ctx.hyper
+        mom = h.momentum > 0
+        dev = ctx.device
+        new = lambda shape: torch.empty(shape, dtype=ctx.dtype, device=dev)  # noqa: E731
+        zero = lambda shape: torch.zeros(shape, dtype=ctx.dtype, device=dev)  # noqa: E731
+        dP = [zero(sh) if c is None else c.contiguous() for c, sh in zip(cots[:S], ctx.shapes)]
+        dT = None
+        if mom and any(c is not None for c in cots[S:2 * S]):
+            dT = [zero(sh) if c is None else c.contiguous() for c, sh in zip(cots[S:2 * S], ctx.shapes)]
+        dg = [new(sh) for sh in ctx.shapes]
+        dt = [new(sh) for sh in ctx.shapes] if mom else None
+        _d.sgd_bwd_tree(ctx.table, _ptrs_or_none(dP, dev), _ptrs_or_none(dT, dev), h.lr, h.momentum, h.nesterov,
+                        _ptrs_or_none(dg, dev), _ptrs_or_none(dt, dev))
+        # the params path is the identity: the cotangent of each p leaf is dP
+        grads = [*dP, *dg]
+        if ctx.has_trace:
+            grads += dt if mom else [None] * S
+        return (None, None, None, *grads)
+
+
+class RMSPropTreeFn(torch.autograd.Function):
+    """Leaf-direct differentiable RMSProp step (momentum optional).
+
+    apply(table, hyper, has_mom, *leaves) with leaves = p_1..p_S, g_1..g_S,
+    v_1..v_S and, when has_mom, the momentum buffer b_1..b_S; returns
+    p'_1..p'_S, v'_1..v'_S and, when momentum > 0, b'_1..b'_S.  The VJP
+    (reduced form, Sec. 2.3) uses the saved g and v."""
+
+    @staticmethod
+    def forward(ctx, table, hyper: RMSPropHyper, has_mom: bool, *leaves):
+        S = len(table.numel)
+        p, g, v = ([x.contiguous() for x in leaves[i * S:(i + 1) * S]] for i in range(3))
+        b = [x.contiguous() for x in leaves[3 * S:4 * S]] if has_mom else None
+        mom = hyper.momentum > 0
+        dev = p[0].device
+        po = [torch.empty_like(x) for x in p]
+        vo = [torch.empty_like(x) for x in v]
+        bo = [torch.empty_like(x) for x in p] if mom else None
+        h = hyper
+        _d.rmsprop_fwd_tree(table, _ptrs_or_none(p, dev), _ptrs_or_none(g, dev), _ptrs_or_none(v, dev),
+                            _ptrs_or_none(b, dev), h.lr, h.alpha, h.eps, h.eps_root, h.momentum,
+                            _ptrs_or_none(po, dev), _ptrs_or_none(vo, dev), _ptrs_or_none(bo, dev))
+        ctx.save_for_backward(*g, *v)
+        ctx.table, ctx.hyper, ctx.has_mom, ctx.S = table, hyper, has_mom, S
+        return (*po, *vo, *bo) if mom else (*po, *vo)
+
+    @staticmethod
+    def backward(ctx, *cots):
+        S, h = ctx.S, ctx.hyper
+        mom = h.momentum > 0
+        saved = ctx.saved_tensors
+        g, v = saved[:S], saved[S:]
+        dev = g[0].device
+
+        def cot(group):
+            if all(c is None for c in group):
+                return None
+            return [torch.zeros_like(x) if c is None else c.contiguous() for c, x in zip(group, g)]
+
+        dP = cot(cots[:S]) or [torch.zeros_like(x) for x in g]
+        dV = cot(cots[S:2 * S])
+        dB = cot(cots[2 * S:3 * S]) if mom else None
+        dg = [torch.empty_like(x) for x in g]
+        dv = [torch.empty_like(x) for x in v]
+        db = [torch.empty_like(x) for x in g] if mom else None
+        _d.rmsprop_bwd_tree(ctx.table, _ptrs_or_none(dP, dev), _ptrs_or_none(dV, dev), _ptrs_or_none(dB, dev),
+                            _ptrs_or_none(list(g), dev), _ptrs_or_none(list(v), dev), h.lr, h.alpha, h.eps,
+                            h.eps_root, h.momentum, _ptrs_or_none(dg, dev), _ptrs_or_none(dv, dev),
+                            _ptrs_or_none(db, dev))
+        grads = [*dP, *dg, *dv]
+        if ctx.has_mom:
+            grads += db if mom else [None] * S
+        return (None, None, None, *grads)
+
+
+class MetaSGD(_MetaOptimizer):
+    """Object-oriented differentiable SGD (momentum, Nesterov optional) over a
+    module's parameters; each step is one leaf-direct launch (SGDTreeFn).  The
+    trace starts absent (zero), as torch.optim's first momentum step."""
+
+    def __init__(self, module: torch.nn.Module, lr=0.1, momentum=0.0, nesterov=False):
+        super().__init__(module)
+        self.hyper = SGDHyper(lr, momentum, nesterov)
+        self.trace = None
+
+    def step(self, loss: torch.Tensor) -> None:
+        params = self.params()
+        grads = torch.autograd.grad(loss, params, create_graph=True)
+        has_trace = self.trace is not None
+        out = SGDTreeFn.apply(self.table, self.hyper, has_trace, *params, *grads, *(self.trace or []))
+        S = len(params)
+        self._install(out[:S])
+        if self.hyper.momentum > 0:
+            self.trace = list(out[S:])
+
+    def detach_(self) -> None:
+        self._detach_params()
+        if self.trace is not None:
+            self.trace = [t.detach() for t in self.trace]
+
+
+class MetaRMSProp(_MetaOptimizer):
+    """Object-oriented differentiable RMSProp (momentum optional) over a
+    module's parameters; each step is one leaf-direct launch (RMSPropTreeFn)."""
+
+    def __init__(self, module: torch.nn.Module, lr=1e-2, alpha=0.99, eps=1e-8, eps_root=0.0, momentum=0.0):
+        super().__init__(module)
+        self.hyper = RMSPropHyper(lr, alpha, eps, eps_root, momentum)
+        self.nu = [torch.zeros_like(p) for p in self.params()]
+        self.mom = None
+
+    def step(self, loss: torch.Tensor) -> None:
+        params = self.params()
+        grads = torch.autograd.grad(loss, params, create_graph=True)
+        has_mom = self.mom is not None
+        out = RMSPropTreeFn.apply(self.table, self.hyper, has_mom, *params, *grads, *self.nu, *(self.mom or []))
+        S = len(params)
+        self._install(out[:S])
+        self.nu = list(out[S:2 * S])
+        if self.hyper.momentum > 0:
+            self.mom = list(out[2 * S:])
+
+    def detach_(self) -> None:
+        self._detach_params()
+        self.nu = [v.detach() for v in self.nu]
+        if self.mom is not None:
+            self.mom = [b.detach() for b in self.mom]
 
 
 def es_gradient(fn, theta: torch.Tensor, sigma: float, num_samples: int, method: str = "antithetic",

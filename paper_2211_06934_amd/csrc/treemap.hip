@@ -16,6 +16,7 @@
 // aligned in every operand takes 128-bit loads and stores; any other group is
 // processed element by element with the same arithmetic.
 #include "adam_math.hpp"
+#include "optim_ops.hpp"
 #include "segtable.hpp"
 
 // Each workgroup covers one table tile (512 groups).  Measured on MI355X
@@ -592,6 +593,74 @@ int launch_trbwd_c(const char* who, int C, const diffopt_segtable* t, const TRBw
 }
 static_assert(kTRS == 8, "launch_trbwd_c instantiates run lengths 1..8");
 
+// ---- leaf-direct SGD-momentum and RMSProp ------------------------------------------
+// The ops of optim_ops.hpp applied leaf by leaf, in the layout of the fused
+// Adam kernels: one table tile per workgroup, one group per lane, the leaf
+// address of every operand staged in the window.  Operands: the op's inputs,
+// then its outputs.
+template <class Op>
+__global__ __launch_bounds__(kUTB) void ew_tree_kernel(const SegEntry* __restrict__ seg,
+                                                      const int64_t* __restrict__ tile_first, int64_t ngroups,
+                                                      int dense_orig, LeafArrays<Op::NIN + Op::NOUT> arr, Op op) {
+  constexpr int NA = Op::NIN + Op::NOUT;
+  __shared__ int64_t s_goff[kWindowMax + 1];
+  __shared__ int64_t s_numel[kWindowMax];
+  __shared__ int s_al[kWindowMax];
+  __shared__ uint64_t s_ptr[NA * kWindowMax];
+  const int64_t b = blockIdx.x;
+  const int W = stage_window_n(seg, tile_first, arr.a, NA, dense_orig, b, s_goff, s_numel, s_ptr, s_al);
+  const int64_t gidx = b * kTileGroups + threadIdx.x;
+  if (gidx >= ngroups) return;
+  const int t = find_leaf(s_goff, W, gidx);
+  const int64_t e0 = 4 * (gidx - s_goff[t]);
+  const int64_t nel = s_numel[t];
+  if (e0 >= nel) return;
+  const uint64_t* P = s_ptr + t;
+  float xi[Op::NIN], yo[Op::NOUT];
+  if (e0 + 4 <= nel && s_al[t]) {
+    const int64_t i = e0 >> 2;
+    f32x4 x[Op::NIN], y[Op::NOUT];
+#pragma unroll
+    for (int a = 0; a < Op::NIN; ++a) x[a] = ld(at<const f32x4>(P[a * kWindowMax], i));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+#pragma unroll
+      for (int a = 0; a < Op::NIN; ++a) xi[a] = x[a][e];
+      op.apply(xi, yo);
+#pragma unroll
+      for (int q = 0; q < Op::NOUT; ++q) y[q][e] = yo[q];
+    }
+#pragma unroll
+    for (int q = 0; q < Op::NOUT; ++q) st(at<f32x4>(P[(Op::NIN + q) * kWindowMax], i), y[q]);
+  } else {
+    const int64_t end = e0 + 4 < nel ? e0 + 4 : nel;
+    for (int64_t i = e0; i < end; ++i) {
+#pragma unroll
+      for (int a = 0; a < Op::NIN; ++a) xi[a] = *at<const float>(P[a * kWindowMax], i);
+      op.apply(xi, yo);
+#pragma unroll
+      for (int q = 0; q < Op::NOUT; ++q) *at<float>(P[(Op::NIN + q) * kWindowMax], i) = yo[q];
+    }
+  }
+}
+
+// Runner of the leaf-direct kernel for the *_variant selectors: every
+// operand is a device array of leaf addresses.
+struct TreeRun {
+  const char* who;
+  const diffopt_segtable* t;
+  hipStream_t st;
+  template <class Op>
+  int go(const Op& op, const void* const* in, const void* const* out) {
+    LeafArrays<Op::NIN + Op::NOUT> arr{};
+    for (int a = 0; a < Op::NIN; ++a) arr.a[a] = static_cast<const uint64_t*>(in[a]);
+    for (int q = 0; q < Op::NOUT; ++q) arr.a[Op::NIN + q] = static_cast<const uint64_t*>(out[q]);
+    hipLaunchKernelGGL((ew_tree_kernel<Op>), dim3((unsigned)t->ntiles), dim3(kUTB), 0, st, t->d_seg,
+                       t->d_tile_first, t->ngroups, t->dense_orig, arr, op);
+    return launch_status(who);
+  }
+};
+
 int check_table(const char* who, const diffopt_segtable* t) {
   if (!t) return fail(DIFFOPT_EINVAL, "%s: table is NULL", who);
   if (t->elem_bytes != 4) return fail(DIFFOPT_EINVAL, "%s: the table must describe fp32 leaves (elem_bytes 4)", who);
@@ -789,4 +858,88 @@ extern "C" int diffopt_adam_unrolled_bwd_tree(const diffopt_segtable* table, int
     if (rc) return rc;
   }
   return DIFFOPT_OK;
+}
+
+// ---- leaf-direct SGD-momentum and RMSProp entry points ---------------------------------
+
+static int check_sgd_hyper(const char* who, double lr, double momentum) {
+  if (!std::isfinite(lr)) return fail(DIFFOPT_EINVAL, "%s: lr must be finite", who);
+  if (!(momentum >= 0.0 && std::isfinite(momentum)))
+    return fail(DIFFOPT_EINVAL, "%s: momentum must be finite and >= 0", who);
+  return DIFFOPT_OK;
+}
+
+extern "C" int diffopt_sgd_fwd_tree(const diffopt_segtable* table, const uint64_t* params, const uint64_t* grad,
+                                    const uint64_t* trace, double lr, double momentum, int32_t nesterov,
+                                    const uint64_t* params_out, const uint64_t* trace_out, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_sgd_fwd_tree";
+  int rc = check_table(who, table);
+  if (rc) return rc;
+  rc = check_sgd_hyper(who, lr, momentum);
+  if (rc) return rc;
+  if (table->ntiles == 0) return DIFFOPT_OK;
+  const bool mom = momentum > 0.0;
+  if (!params || !grad || !params_out || (mom && !trace_out))
+    return fail(DIFFOPT_EINVAL, "%s: null leaf-address array", who);
+  TreeRun run{who, table, as_stream(stream)};
+  return sgd_fwd_variant(run, params, grad, mom ? trace : nullptr, params_out, mom ? trace_out : nullptr, lr,
+                         momentum, nesterov != 0);
+}
+
+extern "C" int diffopt_sgd_bwd_tree(const diffopt_segtable* table, const uint64_t* dparams_out,
+                                    const uint64_t* dtrace_out, double lr, double momentum, int32_t nesterov,
+                                    const uint64_t* dgrad, const uint64_t* dtrace_in, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_sgd_bwd_tree";
+  int rc = check_table(who, table);
+  if (rc) return rc;
+  rc = check_sgd_hyper(who, lr, momentum);
+  if (rc) return rc;
+  if (table->ntiles == 0) return DIFFOPT_OK;
+  const bool mom = momentum > 0.0;
+  if (!dparams_out || !dgrad || (mom && !dtrace_in)) return fail(DIFFOPT_EINVAL, "%s: null leaf-address array", who);
+  TreeRun run{who, table, as_stream(stream)};
+  return sgd_bwd_variant(run, dparams_out, mom ? dtrace_out : nullptr, dgrad, mom ? dtrace_in : nullptr, lr,
+                         momentum, nesterov != 0);
+}
+
+extern "C" int diffopt_rmsprop_fwd_tree(const diffopt_segtable* table, const uint64_t* params, const uint64_t* grad,
+                                        const uint64_t* nu, const uint64_t* mom, double lr, double alpha, double eps,
+                                        double eps_root, double momentum, const uint64_t* params_out,
+                                        const uint64_t* nu_out, const uint64_t* mom_out, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_rmsprop_fwd_tree";
+  int rc = check_table(who, table);
+  if (rc) return rc;
+  RmsCoef c;
+  rc = rms_coef(who, lr, alpha, eps, eps_root, momentum, &c);
+  if (rc) return rc;
+  if (table->ntiles == 0) return DIFFOPT_OK;
+  const bool m = momentum > 0.0;
+  if (!params || !grad || !nu || !params_out || !nu_out || (m && !mom_out))
+    return fail(DIFFOPT_EINVAL, "%s: null leaf-address array", who);
+  TreeRun run{who, table, as_stream(stream)};
+  return rms_fwd_variant(run, params, grad, nu, m ? mom : nullptr, params_out, nu_out, m ? mom_out : nullptr, c, m);
+}
+
+extern "C" int diffopt_rmsprop_bwd_tree(const diffopt_segtable* table, const uint64_t* dparams_out,
+                                        const uint64_t* dnu_out, const uint64_t* dmom_out, const uint64_t* grad,
+                                        const uint64_t* nu, double lr, double alpha, double eps, double eps_root,
+                                        double momentum, const uint64_t* dgrad, const uint64_t* dnu_in,
+                                        const uint64_t* dmom_in, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_rmsprop_bwd_tree";
+  int rc = check_table(who, table);
+  if (rc) return rc;
+  RmsCoef c;
+  rc = rms_coef(who, lr, alpha, eps, eps_root, momentum, &c);
+  if (rc) return rc;
+  if (table->ntiles == 0) return DIFFOPT_OK;
+  const bool m = momentum > 0.0;
+  if (!dparams_out || !grad || !nu || !dgrad || !dnu_in || (m && !dmom_in))
+    return fail(DIFFOPT_EINVAL, "%s: null leaf-address array", who);
+  TreeRun run{who, table, as_stream(stream)};
+  return rms_bwd_variant(run, dparams_out, dnu_out, m ? dmom_out : nullptr, grad, nu, dgrad, dnu_in,
+                         m ? dmom_in : nullptr, c, m);
 }

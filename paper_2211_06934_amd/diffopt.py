@@ -60,6 +60,11 @@ def _load_library():
         "diffopt_sgd_bwd": (ctypes.c_int, [vp, vp, i64, f64, f64, i32, vp, vp, vp]),
         "diffopt_rmsprop_fwd": (ctypes.c_int, [vp, vp, vp, vp, i64, f64, f64, f64, f64, f64, vp, vp, vp, vp]),
         "diffopt_rmsprop_bwd": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, f64, f64, f64, f64, f64, vp, vp, vp, vp]),
+        "diffopt_sgd_fwd_tree": (ctypes.c_int, [vp, vp, vp, vp, f64, f64, i32, vp, vp, vp]),
+        "diffopt_sgd_bwd_tree": (ctypes.c_int, [vp, vp, vp, f64, f64, i32, vp, vp, vp]),
+        "diffopt_rmsprop_fwd_tree": (ctypes.c_int, [vp, vp, vp, vp, vp, f64, f64, f64, f64, f64, vp, vp, vp, vp]),
+        "diffopt_rmsprop_bwd_tree": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, f64, f64, f64, f64, f64, vp, vp, vp,
+                                                    vp]),
         "diffopt_es_perturb": (ctypes.c_int, [vp, vp, i64, i64, f64, i32, vp, vp]),
         "diffopt_es_estimate": (ctypes.c_int, [vp, vp, i64, i64, f64, vp, vp]),
     }
@@ -386,6 +391,50 @@ def rmsprop_bwd(dparams_out, dnu_out, dmom_out, grad, nu, lr, alpha, eps, eps_ro
                                     _addr(nu, "nu", n=n), int(n), float(lr), float(alpha), float(eps),
                                     float(eps_root), float(momentum), _addr(dgrad, "dgrad", n=n),
                                     _addr(dnu_in, "dnu_in", n=n), _addr(dmom_in, "dmom_in", n=n), _stream(stream)))
+
+
+def sgd_fwd_tree(table: SegTable, params, grad, trace, lr, momentum, nesterov, params_out, trace_out=None,
+                 stream=None) -> None:
+    """diffopt_sgd_fwd_tree; every operand a device int64 array of leaf addresses (trace may be None)."""
+    k = len(table.numel)
+    _check(_lib.diffopt_sgd_fwd_tree(
+        table.handle, _leaf_array(params, "params", k), _leaf_array(grad, "grad", k), _leaf_array(trace, "trace", k),
+        float(lr), float(momentum), int(bool(nesterov)), _leaf_array(params_out, "params_out", k),
+        _leaf_array(trace_out, "trace_out", k), _stream(stream)))
+
+
+def sgd_bwd_tree(table: SegTable, dparams_out, dtrace_out, lr, momentum, nesterov, dgrad, dtrace_in=None,
+                 stream=None) -> None:
+    """diffopt_sgd_bwd_tree (dtrace_out may be None)."""
+    k = len(table.numel)
+    _check(_lib.diffopt_sgd_bwd_tree(
+        table.handle, _leaf_array(dparams_out, "dparams_out", k), _leaf_array(dtrace_out, "dtrace_out", k),
+        float(lr), float(momentum), int(bool(nesterov)), _leaf_array(dgrad, "dgrad", k),
+        _leaf_array(dtrace_in, "dtrace_in", k), _stream(stream)))
+
+
+def rmsprop_fwd_tree(table: SegTable, params, grad, nu, mom, lr, alpha, eps, eps_root, momentum, params_out, nu_out,
+                     mom_out=None, stream=None) -> None:
+    """diffopt_rmsprop_fwd_tree (mom may be None)."""
+    k = len(table.numel)
+    _check(_lib.diffopt_rmsprop_fwd_tree(
+        table.handle, *[_leaf_array(x, w, k) for x, w in ((params, "params"), (grad, "grad"), (nu, "nu"),
+                                                           (mom, "mom"))],
+        float(lr), float(alpha), float(eps), float(eps_root), float(momentum),
+        *[_leaf_array(x, w, k) for x, w in ((params_out, "params_out"), (nu_out, "nu_out"), (mom_out, "mom_out"))],
+        _stream(stream)))
+
+
+def rmsprop_bwd_tree(table: SegTable, dparams_out, dnu_out, dmom_out, grad, nu, lr, alpha, eps, eps_root, momentum,
+                     dgrad, dnu_in, dmom_in=None, stream=None) -> None:
+    """diffopt_rmsprop_bwd_tree (dnu_out / dmom_out may be None)."""
+    k = len(table.numel)
+    _check(_lib.diffopt_rmsprop_bwd_tree(
+        table.handle, *[_leaf_array(x, w, k) for x, w in ((dparams_out, "dparams_out"), (dnu_out, "dnu_out"),
+                                                           (dmom_out, "dmom_out"), (grad, "grad"), (nu, "nu"))],
+        float(lr), float(alpha), float(eps), float(eps_root), float(momentum),
+        *[_leaf_array(x, w, k) for x, w in ((dgrad, "dgrad"), (dnu_in, "dnu_in"), (dmom_in, "dmom_in"))],
+        _stream(stream)))
 
 
 # ---- zero-order (ES) gradient estimation
