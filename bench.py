@@ -106,7 +106,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="many_small",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
-                             "many_small_treemap", "sgd_flat", "rmsprop_flat", "es_resnet18"])
+                             "many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
+                             "es_resnet18"])
     ap.add_argument("--trajectory", choices=["stored", "recompute"], default="recompute",
                     help="K-step driver: store every moment state for the backward, or store only the final one "
                          "(and every %d-th) and let the backward recompute the rest in registers" % REMAT_SPAN)
@@ -128,10 +129,15 @@ KERNEL_SOURCES = {  # the sources each kernel family is built from
     "adam_bwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
     "adam_unrolled_fwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
     "adam_unrolled_bwd_tree": ("treemap.hip", "adam_math.hpp", "segtable.hpp", "common.hpp"),
-    "sgd_fwd": ("optim.hip", "adam_math.hpp", "common.hpp"), "sgd_bwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
-    "rmsprop_fwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
-    "rmsprop_bwd": ("optim.hip", "adam_math.hpp", "common.hpp"),
+    "sgd_fwd": ("optim.hip", "optim_ops.hpp", "adam_math.hpp", "common.hpp"),
+    "sgd_bwd": ("optim.hip", "optim_ops.hpp", "adam_math.hpp", "common.hpp"),
+    "rmsprop_fwd": ("optim.hip", "optim_ops.hpp", "adam_math.hpp", "common.hpp"),
+    "rmsprop_bwd": ("optim.hip", "optim_ops.hpp", "adam_math.hpp", "common.hpp"),
     "es_perturb": ("es.hip", "adam_math.hpp", "common.hpp"), "es_estimate": ("es.hip", "adam_math.hpp", "common.hpp"),
+    "sgd_fwd_tree": ("treemap.hip", "optim_ops.hpp", "adam_math.hpp", "segtable.hpp", "common.hpp"),
+    "sgd_bwd_tree": ("treemap.hip", "optim_ops.hpp", "adam_math.hpp", "segtable.hpp", "common.hpp"),
+    "rmsprop_fwd_tree": ("treemap.hip", "optim_ops.hpp", "adam_math.hpp", "segtable.hpp", "common.hpp"),
+    "rmsprop_bwd_tree": ("treemap.hip", "optim_ops.hpp", "adam_math.hpp", "segtable.hpp", "common.hpp"),
 }
 
 
@@ -352,6 +358,59 @@ def step_optim(P, S, ev=None):
         ev[2].record()
 
 
+def setup_optim_tree(torch, P, which, w):
+    """The same interior step in leaf-direct form over the 20,000-leaf tree:
+    every operand a tree of separately allocated leaves, one launch each."""
+    from workloads import torch_normal
+    n, numel, dev = w.n, w.numels, "cuda"
+    table = P.segtable_create(numel)
+    trees = []
+
+    def tree(seed=None, std=1.0):
+        leaves = [torch.empty(k, dtype=torch.float32, device=dev) for k in numel]
+        if seed is not None:
+            flat = torch_normal(n, std, seed, dev)
+            if which == "rmsprop" and seed == 303:
+                flat.abs_()
+            P.tree_unflatten(table, flat, torch.tensor([x.data_ptr() for x in leaves], dtype=torch.int64).to(dev))
+        trees.append(leaves)
+        return torch.tensor([x.data_ptr() for x in leaves], dtype=torch.int64).to(dev)
+
+    S = dict(K=1, n=n, which=which, table=table, p=tree(301, 0.05), g=tree(302, 0.01), dP=tree(305), po=tree(),
+             dg=tree(), keep=trees)
+    if which == "sgd":
+        S.update(t=tree(303, 0.01), to=tree(), dT=tree(306), dt=tree(), lr=0.05, mom=0.9)
+    else:
+        S.update(v=tree(303, 1e-4), b=tree(304, 0.1), vo=tree(), bo=tree(), dV=tree(306), dB=tree(307), dv=tree(),
+                 db=tree(), lr=1e-3, mom=0.9)
+    torch.cuda.synchronize()
+    return S
+
+
+def step_optim_tree(P, S, ev=None):
+    T = S["table"]
+    if ev:
+        ev[0].record()
+    if S["which"] == "sgd":
+        P.sgd_fwd_tree(T, S["p"], S["g"], S["t"], S["lr"], S["mom"], True, S["po"], S["to"])
+    else:
+        P.rmsprop_fwd_tree(T, S["p"], S["g"], S["v"], S["b"], S["lr"], 0.99, 1e-8, 0.0, S["mom"], S["po"], S["vo"],
+                           S["bo"])
+    if ev:
+        ev[1].record()
+    if S["which"] == "sgd":
+        P.sgd_bwd_tree(T, S["dP"], S["dT"], S["lr"], S["mom"], True, S["dg"], S["dt"])
+    else:
+        P.rmsprop_bwd_tree(T, S["dP"], S["dV"], S["dB"], S["g"], S["v"], S["lr"], 0.99, 1e-8, 0.0, S["mom"],
+                           S["dg"], S["dv"], S["db"])
+    if ev:
+        ev[2].record()
+
+
+def phases_optim_tree(S):
+    return [(name + "_tree", kern + "_tree", 1, b) for name, kern, _, b in phases_optim(S)]
+
+
 def phases_optim(S):
     n = S["n"]
     if S["which"] == "sgd":  # fwd: p, g, t -> p', t'; bwd: dP, dT -> dg, dt
@@ -497,9 +556,12 @@ def main():
         sys.stderr.write("bench.py: no GPU visible\n")
         sys.exit(1)
     w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
+                   "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
                    "es_resnet18": "resnet18_k1"}.get(a.workload, a.workload)]()
     if a.workload == "es_resnet18":
         S, step, phases = setup_es(torch, P, w), step_es, phases_es
+    elif a.workload in ("sgd_treemap", "rmsprop_treemap"):
+        S, step, phases = setup_optim_tree(torch, P, a.workload.split("_")[0], w), step_optim_tree, phases_optim_tree
     elif a.workload in ("sgd_flat", "rmsprop_flat"):
         S, step, phases = setup_optim(torch, P, a.workload.split("_")[0]), step_optim, phases_optim
     elif a.workload == "flat_1b":
@@ -577,7 +639,8 @@ def main():
                     "avg_launch_us": round(avg_launch_s * 1e6, 2)}
 
     cpu = None
-    if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "es_resnet18"):
+    if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap",
+                                                    "rmsprop_treemap", "es_resnet18"):
         cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
         cpu["value"] = float("%.4g" % cpu["value"])
 
@@ -591,11 +654,20 @@ def main():
                            "leaf-direct K=%d unrolled Adam fwd+bwd (no pack/unpack)" % K),
                        "sgd_flat": "flat fp32 buffer, n=%d, one Nesterov SGD-momentum fwd + bwd" % n,
                        "rmsprop_flat": "flat fp32 buffer, n=%d, one RMSProp-momentum fwd + bwd" % n,
+                       "sgd_treemap": "many-small-tensor tree (20000 leaves, n=%d), one leaf-direct Nesterov "
+                                      "SGD-momentum fwd + bwd" % n,
+                       "rmsprop_treemap": "many-small-tensor tree (20000 leaves, n=%d), one leaf-direct "
+                                          "RMSProp-momentum fwd + bwd" % n,
                        "es_resnet18": "ES gradient estimate for n=%d (ResNet-18 size), 64 antithetic samples" % n,
                    }.get(a.workload, w.description),
                    "n_params": n, "leaves": w.nseg, "K": K,
                    "step": {"flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",
-                            "many_small_treemap": "leaf-direct K-step Adam fwd -> K-step Adam bwd (no flatten)"}.get(
+                            "many_small_treemap": "leaf-direct K-step Adam fwd -> K-step Adam bwd (no flatten)",
+                            "sgd_flat": "one SGD fwd + one SGD bwd on the flat buffer",
+                            "rmsprop_flat": "one RMSProp fwd + one RMSProp bwd on the flat buffer",
+                            "sgd_treemap": "leaf-direct SGD fwd -> SGD bwd (no flatten)",
+                            "rmsprop_treemap": "leaf-direct RMSProp fwd -> RMSProp bwd (no flatten)",
+                            "es_resnet18": "perturb theta into 2N points -> ES estimate from N given loss weights"}.get(
                                 a.workload,
                                 "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg"),
                    "launch": "hip graph replay" if a.graph else "eager", "parallelism": "single GPU",
