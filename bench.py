@@ -513,8 +513,20 @@ def cpu_baseline_tree(w, target_s):
                   "unpack p_K + %d cotangents; fp64 single thread; %.1f s"
                   % (nleaves, len(numel), n, w.n, w.K, w.K, w.K, t),
         "seconds": t,
-        "host_cpu": platform.processor() or platform.machine(),
+        "host_cpu": host_cpu_model(), "host_threads": os.cpu_count(),
     }
+
+
+def host_cpu_model():
+    """The host CPU's model name (first processor entry of /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def cpu_baseline_flat_1b(w, target_s):
@@ -537,7 +549,7 @@ def cpu_baseline_flat_1b(w, target_s):
     t = run(n)
     return {"value": n / t, "unit": "params/s", "cores": 1, "kind": "oracle",
             "sample": "first %d of %d params, one fwd+bwd step; fp64 single thread; %.1f s" % (n, w.n, t),
-            "seconds": t, "host_cpu": platform.processor() or platform.machine()}
+            "seconds": t, "host_cpu": host_cpu_model(), "host_threads": os.cpu_count()}
 
 
 # ---------------------------------------------------------------------- main
