@@ -135,7 +135,11 @@ class _MetaOptimizer:
         from .tree import segment_table
         self.module = module
         self.names = [n for n, p in module.named_parameters() if p.requires_grad]
+        if not self.names:
+            raise ValueError("the module has no trainable parameters")
         params = [self._get(n) for n in self.names]
+        if any(p.dtype != torch.float32 or p.device != params[0].device for p in params):
+            raise ValueError("the fused optimizers take fp32 parameters on one device")
         self.table = segment_table([tuple(p.shape) for p in params], params[0].dtype, params[0].device)
 
     def _owner(self, name):
