@@ -4,6 +4,8 @@
   explicit-gradient loop, its meta-gradient via torch.autograd.grad against
   the oracle's K-step backward;
 - capture of the unrolled forward + backward in a HIP graph (torch.cuda.graph),
+  and of every other launching entry point (batched copies, leaf-direct
+  drivers and optimizers, ES) in one captured sequence,
   replayed several times with eager work in between, every replay compared
   with the eager result (the library allocates and synchronises nothing on
   the path, so it is capture-safe).
@@ -146,3 +148,70 @@ def test_tree_flatten_in_hip_graph_replays():
         torch.cuda.synchronize()
         assert torch.equal(flat, ref), rep
         assert all(torch.equal(a, b) for a, b in zip(outs, leaves)), rep
+
+
+def test_leaf_direct_and_batched_entry_points_in_hip_graph_replay():
+    # every other launching entry point in one captured sequence: batched
+    # pack/unpack, the leaf-direct K-step driver (trajectory recomputed),
+    # leaf-direct SGD-momentum and RMSProp, and the ES perturb/estimate pair;
+    # each replay must equal the eager run bit for bit
+    import paper_2211_06934_amd as P
+    w = WORKLOADS["resnet18_k1"]()
+    numel, n, K = w.numels, w.n, 3
+    table = P.segtable_create(numel)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    rnd = lambda std=1.0: [torch.randn(k, device="cuda", generator=gen) * std for k in numel]  # noqa: E731
+    emp = lambda: [torch.empty(k, device="cuda") for k in numel]  # noqa: E731
+    ptr = lambda leaves: torch.tensor([x.data_ptr() for x in leaves], dtype=torch.int64, device="cuda")  # noqa: E731
+    p, cot, t, dT = rnd(0.05), rnd(), rnd(0.01), rnd()
+    gs = [rnd(0.01) for _ in range(K)]
+    v = [x.abs() for x in rnd(1e-4)]
+    z = [torch.zeros(k, device="cuda") for k in numel]
+    trees = dict(p=p, cot=cot, t=t, dT=dT, v=v, z=z, **{"g%d" % k: gs[k] for k in range(K)})
+    out = {k: emp() for k in ("pK", "muK", "nuK", "dm0", "dv0", "po", "to", "dg_s", "dt", "rpo", "rvo", "rdg", "rdv",
+                              "unp", *("dg%d" % k for k in range(K)))}
+    P_ = {k: ptr(x) for k, x in {**trees, **out}.items()}
+    flats = [torch.empty(n, device="cuda") for _ in range(K + 1)]
+    theta, noise = torch.randn(4096, device="cuda", generator=gen), torch.randn(8, 4096, device="cuda", generator=gen)
+    wts = torch.randn(8, device="cuda", generator=gen)
+    pts, eg = torch.empty(16, 4096, device="cuda"), torch.empty(4096, device="cuda")
+
+    def run():
+        P.tree_flatten_batch(table, [P_["p"]] + [P_["g%d" % k] for k in range(K)], flats)
+        P.tree_unflatten_batch(table, [flats[0]], [P_["unp"]])
+        mt = [P_["z"]] + [None] * (K - 1) + [P_["muK"]]
+        vt = [P_["z"]] + [None] * (K - 1) + [P_["nuK"]]
+        gl = [P_["g%d" % k] for k in range(K)]
+        P.adam_unrolled_fwd_tree(table, P_["p"], gl, mt, vt, P_["pK"], 0, LR, B1, B2, EPS, 1e-8)
+        P.adam_unrolled_bwd_tree(table, P_["cot"], gl, mt, vt, [P_["dg%d" % k] for k in range(K)], P_["dm0"],
+                                 P_["dv0"], 0, LR, B1, B2, EPS, 1e-8)
+        P.sgd_fwd_tree(table, P_["p"], P_["g0"], P_["t"], 0.05, 0.9, True, P_["po"], P_["to"])
+        P.sgd_bwd_tree(table, P_["cot"], P_["dT"], 0.05, 0.9, True, P_["dg_s"], P_["dt"])
+        P.rmsprop_fwd_tree(table, P_["p"], P_["g0"], P_["v"], None, 1e-3, 0.99, 1e-8, 0.0, 0.0, P_["rpo"],
+                           P_["rvo"])
+        P.rmsprop_bwd_tree(table, P_["cot"], P_["dT"], None, P_["g0"], P_["v"], 1e-3, 0.99, 1e-8, 0.0, 0.0,
+                           P_["rdg"], P_["rdv"])
+        P.es_perturb(theta, noise, 0.1, True, pts)
+        P.es_estimate(noise, wts, 0.5, eg)
+
+    run()
+    torch.cuda.synchronize()
+    outs = [x for leaves in out.values() for x in leaves] + flats + [pts, eg]
+    eager = [x.clone() for x in outs]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        run()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    for rep in range(3):
+        for x in outs:
+            x.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(outs, eager)):
+            assert torch.equal(a, b), (rep, i)
