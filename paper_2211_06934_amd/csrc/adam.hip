@@ -51,6 +51,18 @@
 #ifndef DIFFOPT_URBWD_BLOCK_LONG
 #define DIFFOPT_URBWD_BLOCK_LONG 256
 #endif
+// Arrays of fewer than DIFFOPT_SMALL_VECS 16-byte vectors take workgroups of
+// at most DIFFOPT_SMALL_BLOCK threads in the fused K-step kernels: with few
+// large workgroups per CU, the last round of workgroups leaves CUs idle.
+// Measured (graph replay, pack -> K steps -> unpack): ResNet-18 tree
+// (1.17e7 params) K = 1 183 -> 178-179 us; K = 10 and the 3.6e6-param
+// conv-net within 1% (128 threads: the same within noise, 512: no better).
+#ifndef DIFFOPT_SMALL_VECS
+#define DIFFOPT_SMALL_VECS (1 << 22)
+#endif
+#ifndef DIFFOPT_SMALL_BLOCK
+#define DIFFOPT_SMALL_BLOCK 256
+#endif
 
 namespace diffopt {
 
@@ -285,6 +297,9 @@ __global__ __launch_bounds__(kAB) void adam_bwd_scalar(const float* dP, const fl
 constexpr int kUK = 16;  // steps per fused launch (kernel-argument space bounds it)
 constexpr int kUFB = DIFFOPT_UFWD_BLOCK;
 constexpr int kUBB = DIFFOPT_UBWD_BLOCK;
+constexpr int kSmallB = DIFFOPT_SMALL_BLOCK;
+constexpr int64_t kSmallVecs = DIFFOPT_SMALL_VECS;
+static_assert(kSmallB >= 64 && kSmallB % 64 == 0, "whole wavefronts; the tail needs 4 lanes");
 
 // Step s of a launch is the launch's s-th step in execution order.
 struct UFwdArgs {
@@ -359,11 +374,12 @@ __device__ __forceinline__ void ufwd_element(int64_t e, const UFwdArgs& a) {
 // Tile t covers 16-byte vectors [t B, (t+1) B) for B threads per workgroup;
 // only the last tile checks bounds, and the last workgroup also runs the
 // n % 4 tail elements.
-__global__ __launch_bounds__(kUFB) void adam_unrolled_fwd_vec(UFwdArgs a) {
+template <int B>
+__global__ __launch_bounds__(B) void adam_unrolled_fwd_vec(UFwdArgs a) {
   const int64_t nv = a.n >> 2;
-  const int64_t ntiles = (nv + kUFB - 1) / kUFB;
+  const int64_t ntiles = (nv + B - 1) / B;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t i = t * kUFB + threadIdx.x;
+    const int64_t i = t * B + threadIdx.x;
     if (i < nv) ufwd_vector(i, a);
   }
   if (blockIdx.x == gridDim.x - 1) {
@@ -453,11 +469,12 @@ __device__ __forceinline__ void ubwd_element(int64_t e, const UBwdArgs& a) {
   a.dv[e] = dV;
 }
 
-__global__ __launch_bounds__(kUBB) void adam_unrolled_bwd_vec(UBwdArgs a) {
+template <int B>
+__global__ __launch_bounds__(B) void adam_unrolled_bwd_vec(UBwdArgs a) {
   const int64_t nv = a.n >> 2;
-  const int64_t ntiles = (nv + kUBB - 1) / kUBB;
+  const int64_t ntiles = (nv + B - 1) / B;
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const int64_t i = t * kUBB + threadIdx.x;
+    const int64_t i = t * B + threadIdx.x;
     if (i < nv) ubwd_vector(i, a);
   }
   if (blockIdx.x == gridDim.x - 1) {
@@ -596,7 +613,11 @@ __global__ __launch_bounds__(B) void adam_unrolled_bwd_remat_elem(URBwdArgs a) {
 template <int C>
 void launch_urbwd(bool vec, const URBwdArgs& a, hipStream_t st) {
   constexpr int B = C >= DIFFOPT_URBWD_LONG_RUN ? DIFFOPT_URBWD_BLOCK_LONG : kURB;
-  if (vec)
+  constexpr int BS = B < kSmallB ? B : kSmallB;
+  if (vec && (a.n >> 2) < kSmallVecs)
+    hipLaunchKernelGGL((adam_unrolled_bwd_remat_vec<C, BS>), dim3((unsigned)grid_for(((a.n >> 2) + BS - 1) / BS)),
+                       dim3(BS), 0, st, a);
+  else if (vec)
     hipLaunchKernelGGL((adam_unrolled_bwd_remat_vec<C, B>), dim3((unsigned)grid_for(((a.n >> 2) + B - 1) / B)),
                        dim3(B), 0, st, a);
   else
@@ -775,9 +796,12 @@ extern "C" int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0, 
       a.m[a.K - 1] = mu_traj[K];
       a.v[a.K - 1] = nu_traj[K];
     }
-    if (vec)
-      hipLaunchKernelGGL(adam_unrolled_fwd_vec, dim3((unsigned)grid_for(((n >> 2) + kUFB - 1) / kUFB)), dim3(kUFB),
-                         0, st, a);
+    if (vec && (n >> 2) < kSmallVecs)
+      hipLaunchKernelGGL((adam_unrolled_fwd_vec<kSmallB>), dim3((unsigned)grid_for(((n >> 2) + kSmallB - 1) / kSmallB)),
+                         dim3(kSmallB), 0, st, a);
+    else if (vec)
+      hipLaunchKernelGGL((adam_unrolled_fwd_vec<kUFB>), dim3((unsigned)grid_for(((n >> 2) + kUFB - 1) / kUFB)),
+                         dim3(kUFB), 0, st, a);
     else  // some pointer is not 16-byte aligned: one element per lane, same arithmetic
       hipLaunchKernelGGL(adam_unrolled_fwd_elem, dim3((unsigned)grid_for((n + kUFB - 1) / kUFB)), dim3(kUFB), 0, st,
                          a);
@@ -838,8 +862,11 @@ extern "C" int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
         if (on) make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &a.c[s]);
         else a.c[s] = AdamCoef{};
       }
-      if (vec)
-        hipLaunchKernelGGL(adam_unrolled_bwd_vec, dim3((unsigned)grid_for(((n >> 2) + kUBB - 1) / kUBB)),
+      if (vec && (n >> 2) < kSmallVecs)
+        hipLaunchKernelGGL((adam_unrolled_bwd_vec<kSmallB>),
+                           dim3((unsigned)grid_for(((n >> 2) + kSmallB - 1) / kSmallB)), dim3(kSmallB), 0, st, a);
+      else if (vec)
+        hipLaunchKernelGGL((adam_unrolled_bwd_vec<kUBB>), dim3((unsigned)grid_for(((n >> 2) + kUBB - 1) / kUBB)),
                            dim3(kUBB), 0, st, a);
       else
         hipLaunchKernelGGL(adam_unrolled_bwd_elem, dim3((unsigned)grid_for((n + kUBB - 1) / kUBB)), dim3(kUBB), 0,
