@@ -1,0 +1,150 @@
+"""The benchmark's own timed steps, at full size, against the oracle.
+
+bench.py's setup and step functions are called as they are (same leaves,
+same batched copies, same store policy and launch plan), and the outputs are
+compared with the oracle on a seeded sample of elements: every operation on
+the path is elementwise (the copies move each element on its own), so the
+oracle computes any sampled element from that element's inputs alone.
+
+  - pack and unpack: the flat buffers equal the concatenated leaves bit for
+    bit (checked in full on the device);
+  - forward: p_K per element within 1e-5 of its term scale, propagated over
+    the K steps of the all-fp64 run; the final moments norm-relative 1e-5;
+  - VJP: every dg_k, dmu0, dnu0 against the all-fp64 oracle from the same
+    fp32 inputs, norm-relative 1e-4 (the moment trajectory is recomputed on
+    the GPU, so the end-to-end reading applies).
+"""
+import importlib.util
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.support import BWD_RTOL, FWD_RTOL, assert_mag_close, stats
+from workloads import WORKLOADS
+
+pytestmark = pytest.mark.gpu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _bench():
+    spec = importlib.util.spec_from_file_location("bench_under_test", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def _sample(n, count, seed):
+    rng = np.random.default_rng(seed)
+    idx = np.concatenate([np.arange(min(n, 1024)), np.arange(max(0, n - 1024), n), rng.integers(0, n, size=count)])
+    return torch.from_numpy(np.unique(idx)).cuda()
+
+
+def _cat(leaves):
+    return torch.cat([x.reshape(-1) for x in leaves])
+
+
+def _check_adam(S, flat, idx):
+    """flat: dict of full-size flat device buffers p0, g (list), cot, pK, muK,
+    nuK, dg (list), dm0, dv0 as the step left them."""
+    K, h = S["K"], S["hyper"]
+    hp = (h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+    at = lambda t: t.index_select(0, idx).cpu().numpy().astype(np.float64)  # noqa: E731
+    p0, cot = at(flat["p0"]), at(flat["cot"])
+    G = np.stack([at(g) for g in flat["g"]])
+    z = np.zeros_like(p0)
+    pK_ref, mt_ref, vt_ref = oracle.unrolled_fwd(p0, G, z, z, S["count0"], *hp)
+    mag_p = np.abs(p0)
+    for k in range(1, K + 1):
+        mag_p = mag_p + oracle.adam_fwd_mag(p0, G[k - 1], mt_ref[k - 1], vt_ref[k - 1], S["count0"] + k - 1, *hp)[3]
+    assert_mag_close(at(flat["pK"]), pK_ref, mag_p, FWD_RTOL, "p_K")
+    assert stats(at(flat["muK"]), mt_ref[K])[1] < FWD_RTOL, "mu_K"
+    assert stats(at(flat["nuK"]), vt_ref[K])[1] < FWD_RTOL, "nu_K"
+    _, dg_r, dm0_r, dv0_r = oracle.unrolled_bwd(cot, G, mt_ref, vt_ref, S["count0"], *hp)
+    for k in range(K):
+        assert stats(at(flat["dg"][k]), dg_r[k])[1] < BWD_RTOL, "dg_%d" % k
+    assert stats(at(flat["dm0"]), dm0_r)[1] < BWD_RTOL, "dmu0"
+    assert stats(at(flat["dv0"]), dv0_r)[1] < BWD_RTOL, "dnu0"
+
+
+@pytest.mark.parametrize("name", ["many_small", "resnet18_k10"])
+def test_flatten_fused_unflatten_step(name):
+    import paper_2211_06934_amd as P
+    b = _bench()
+    w = WORKLOADS[name]()
+    S = b.setup_tree(torch, P, w, "recompute")
+    b.step_tree(P, S)
+    torch.cuda.synchronize()
+    p_tree, g_trees, pK_tree, dg_trees = S["keep"]
+    K = S["K"]
+    # the copies: flat inputs are the packed leaves, unpacked outputs the flat results
+    assert torch.equal(S["p0"].view(torch.int32), _cat(p_tree).view(torch.int32))
+    for k in range(K):
+        assert torch.equal(S["g"][k].view(torch.int32), _cat(g_trees[k]).view(torch.int32)), k
+        assert torch.equal(S["dg"][k].view(torch.int32), _cat(dg_trees[k]).view(torch.int32)), k
+    assert torch.equal(S["pK"].view(torch.int32), _cat(pK_tree).view(torch.int32))
+    flat = dict(p0=S["p0"], g=S["g"], cot=S["cot"], pK=S["pK"], muK=S["mu"][K], nuK=S["nu"][K], dg=S["dg"],
+                dm0=S["dm0"], dv0=S["dv0"])
+    _check_adam(S, flat, _sample(S["n"], 200_000, 11))
+
+
+def test_leaf_direct_step():
+    import paper_2211_06934_amd as P
+    b = _bench()
+    S = b.setup_treemap(torch, P, WORKLOADS["many_small"](), "recompute")
+    b.step_treemap(P, S)
+    torch.cuda.synchronize()
+    n, K = S["n"], S["K"]
+
+    def flat(ptrs):
+        out = torch.empty(n, device="cuda")
+        P.tree_flatten(S["table"], ptrs, out)
+        return out
+
+    fl = dict(p0=flat(S["p0"]), g=[flat(g) for g in S["g"]], cot=flat(S["cot"]), pK=flat(S["pK"]),
+              muK=flat(S["mu"][K]), nuK=flat(S["nu"][K]), dg=[flat(d) for d in S["dg"]], dm0=flat(S["dm0"]),
+              dv0=flat(S["dv0"]))
+    torch.cuda.synchronize()
+    _check_adam(S, fl, _sample(n, 200_000, 12))
+
+
+@pytest.mark.parametrize("which", ["sgd", "rmsprop"])
+def test_leaf_direct_sgd_rmsprop_step(which):
+    import paper_2211_06934_amd as P
+    b = _bench()
+    S = b.setup_optim_tree(torch, P, which, WORKLOADS["many_small"]())
+    b.step_optim_tree(P, S)
+    torch.cuda.synchronize()
+    n = S["n"]
+    idx = _sample(n, 200_000, 13)
+
+    def at(ptrs):
+        out = torch.empty(n, device="cuda")
+        P.tree_flatten(S["table"], ptrs, out)
+        return out.index_select(0, idx).cpu().numpy().astype(np.float64)
+
+    p, g, dP = at(S["p"]), at(S["g"]), at(S["dP"])
+    if which == "sgd":
+        t, dT = at(S["t"]), at(S["dT"])
+        ref = oracle.sgd_fwd(p, g, t, S["lr"], S["mom"], True)
+        mag = oracle.sgd_fwd_mag(p, g, t, S["lr"], S["mom"], True)
+        for got, r, m, what in zip((at(S["po"]), at(S["to"])), ref, mag, ("p'", "t'")):
+            assert_mag_close(got, r, m, FWD_RTOL, what)
+        ref = oracle.sgd_bwd(dP, dT, S["lr"], S["mom"], True)[1:]  # (dg, dt)
+        mag = oracle.sgd_bwd_mag(dP, dT, S["lr"], S["mom"], True)
+        for got, r, m, what in zip((at(S["dg"]), at(S["dt"])), ref, mag, ("dg", "dt")):
+            assert_mag_close(got, r, m, BWD_RTOL, what)
+    else:
+        v, bb, dV, dB = at(S["v"]), at(S["b"]), at(S["dV"]), at(S["dB"])
+        hp = (S["lr"], 0.99, 1e-8, 0.0, S["mom"])
+        ref = oracle.rmsprop_fwd(p, g, v, bb, *hp)
+        mag = oracle.rmsprop_fwd_mag(p, g, v, bb, *hp)
+        for got, r, m, what in zip((at(S["po"]), at(S["vo"]), at(S["bo"])), ref, mag, ("p'", "v'", "b'")):
+            assert_mag_close(got, r, m, FWD_RTOL, what)
+        ref = oracle.rmsprop_bwd(dP, dV, dB, g, v, *hp)[1:]  # (dg, dv, db)
+        mag = oracle.rmsprop_bwd_mag(dP, dV, dB, g, v, *hp)
+        for got, r, m, what in zip((at(S["dg"]), at(S["dv"]), at(S["db"])), ref, mag, ("dg", "dv", "db")):
+            assert_mag_close(got, r, m, BWD_RTOL, what)
