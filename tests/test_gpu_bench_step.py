@@ -1,4 +1,6 @@
-"""The benchmark's own timed steps, at full size, against the oracle.
+"""The benchmark's own timed steps (every workload it offers but the flat 10^9
+case, which tests/test_gpu_unrolled.py covers in its own launch configuration),
+at full size, against the oracle.
 
 bench.py's setup and step functions are called as they are (same leaves,
 same batched copies, same store policy and launch plan), and the outputs are
@@ -70,7 +72,7 @@ def _check_adam(S, flat, idx):
     assert stats(at(flat["dv0"]), dv0_r)[1] < BWD_RTOL, "dnu0"
 
 
-@pytest.mark.parametrize("name", ["many_small", "resnet18_k10"])
+@pytest.mark.parametrize("name", ["many_small", "resnet18_k10", "resnet18_k1", "convnet32", "tiny_mlp"])
 def test_flatten_fused_unflatten_step(name):
     import paper_2211_06934_amd as P
     b = _bench()
@@ -148,3 +150,53 @@ def test_leaf_direct_sgd_rmsprop_step(which):
         mag = oracle.rmsprop_bwd_mag(dP, dV, dB, g, v, *hp)
         for got, r, m, what in zip((at(S["dg"]), at(S["dv"]), at(S["db"])), ref, mag, ("dg", "dv", "db")):
             assert_mag_close(got, r, m, BWD_RTOL, what)
+
+
+@pytest.mark.parametrize("which", ["sgd", "rmsprop"])
+def test_flat_sgd_rmsprop_step(which):
+    import paper_2211_06934_amd as P
+    b = _bench()
+    S = b.setup_optim(torch, P, which)
+    b.step_optim(P, S)
+    torch.cuda.synchronize()
+    idx = _sample(S["n"], 200_000, 14)
+    at = lambda t: t.index_select(0, idx).cpu().numpy().astype(np.float64)  # noqa: E731
+    p, g, dP = at(S["p"]), at(S["g"]), at(S["dP"])
+    if which == "sgd":
+        t, dT = at(S["t"]), at(S["dT"])
+        fwd = zip((at(S["po"]), at(S["to"])), oracle.sgd_fwd(p, g, t, S["lr"], S["mom"], True),
+                  oracle.sgd_fwd_mag(p, g, t, S["lr"], S["mom"], True))
+        bwd = zip((at(S["dg"]), at(S["dt"])), oracle.sgd_bwd(dP, dT, S["lr"], S["mom"], True)[1:],
+                  oracle.sgd_bwd_mag(dP, dT, S["lr"], S["mom"], True))
+    else:
+        v, bb, dV, dB = at(S["v"]), at(S["b"]), at(S["dV"]), at(S["dB"])
+        hp = (S["lr"], 0.99, 1e-8, 0.0, S["mom"])
+        fwd = zip((at(S["po"]), at(S["vo"]), at(S["bo"])), oracle.rmsprop_fwd(p, g, v, bb, *hp),
+                  oracle.rmsprop_fwd_mag(p, g, v, bb, *hp))
+        bwd = zip((at(S["dg"]), at(S["dv"]), at(S["db"])), oracle.rmsprop_bwd(dP, dV, dB, g, v, *hp)[1:],
+                  oracle.rmsprop_bwd_mag(dP, dV, dB, g, v, *hp))
+    for i, (got, r, m) in enumerate(fwd):
+        assert_mag_close(got, r, m, FWD_RTOL, "fwd output %d" % i)
+    for i, (got, r, m) in enumerate(bwd):
+        assert_mag_close(got, r, m, BWD_RTOL, "bwd output %d" % i)
+
+
+def test_es_step():
+    # ResNet-18 size, 64 antithetic rows: sampled columns of the points and
+    # of the estimate (every column is computed from its own column of noise)
+    import paper_2211_06934_amd as P
+    b = _bench()
+    S = b.setup_es(torch, P, WORKLOADS["resnet18_k1"]())
+    b.step_es(P, S)
+    torch.cuda.synchronize()
+    idx = _sample(S["n"], 50_000, 15)
+    cols = lambda t: t.index_select(1, idx).cpu().numpy().astype(np.float64)  # noqa: E731
+    theta = S["theta"].index_select(0, idx).cpu().numpy().astype(np.float64)
+    Z = cols(S["noise"])
+    sigma, N = S["sigma"], S["N"]
+    mag = np.abs(theta)[None, :] + sigma * np.abs(np.concatenate([Z, Z]))
+    assert_mag_close(cols(S["pts"]), oracle.es_perturb(theta, Z, sigma, True), mag, FWD_RTOL, "perturb")
+    w = S["w"].cpu().numpy().astype(np.float64)
+    scale = 1.0 / (2 * N * sigma)
+    g = S["grad"].index_select(0, idx).cpu().numpy().astype(np.float64)
+    assert_mag_close(g, oracle.es_estimate(Z, w, scale), oracle.es_estimate_mag(Z, w, scale), BWD_RTOL, "estimate")
