@@ -90,7 +90,7 @@ class AdamTreeFn(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, table, count: int, hyper: AdamHyper, *leaves):
-        from .tree import leaf_pointer_tensor
+        from .tree import leaf_pointer_tensors
         S = len(leaves) // 4
         p, g, m, v = (list(leaves[i * S:(i + 1) * S]) for i in range(4))
         p, g, m, v = ([x.contiguous() for x in t] for t in (p, g, m, v))
@@ -98,7 +98,7 @@ class AdamTreeFn(torch.autograd.Function):
         po = [torch.empty_like(x) for x in p]
         mo = [torch.empty_like(x) for x in m]
         vo = [torch.empty_like(x) for x in v]
-        ptr = [leaf_pointer_tensor(t, dev) for t in (p, g, m, v, po, mo, vo)]
+        ptr = leaf_pointer_tensors((p, g, m, v, po, mo, vo), dev)
         _d.adam_fwd_tree(table, ptr[0], ptr[1], ptr[2], ptr[3], count, hyper.lr, hyper.b1, hyper.b2, hyper.eps,
                          hyper.eps_root, ptr[4], ptr[5], ptr[6])
         ctx.save_for_backward(*g, *m, *v)
@@ -107,7 +107,7 @@ class AdamTreeFn(torch.autograd.Function):
 
     @staticmethod
     def backward(ctx, *cots):
-        from .tree import leaf_pointer_tensor
+        from .tree import leaf_pointer_tensors
         S, h = ctx.S, ctx.hyper
         saved = ctx.saved_tensors
         g, m, v = saved[:S], saved[S:2 * S], saved[2 * S:]
@@ -118,7 +118,7 @@ class AdamTreeFn(torch.autograd.Function):
         dg = [torch.empty_like(x) for x in g]
         dm = [torch.empty_like(x) for x in m]
         dv = [torch.empty_like(x) for x in v]
-        ptr = [leaf_pointer_tensor(t, dev) for t in (dP, dM, dV, g, m, v, dg, dm, dv)]
+        ptr = leaf_pointer_tensors((dP, dM, dV, g, m, v, dg, dm, dv), dev)
         _d.adam_bwd_tree(ctx.table, ptr[0], ptr[1], ptr[2], ptr[3], ptr[4], ptr[5], ctx.count, h.lr, h.b1, h.b2,
                          h.eps, h.eps_root, ptr[6], ptr[7], ptr[8])
         # the params path is the identity: the cotangent of each p leaf is dP
@@ -223,9 +223,9 @@ class RMSPropHyper:
     momentum: float = 0.0
 
 
-def _ptrs_or_none(leaves, dev):
-    from .tree import leaf_pointer_tensor
-    return None if leaves is None else leaf_pointer_tensor(leaves, dev)
+def _ptrs(groups, dev):
+    from .tree import leaf_pointer_tensors
+    return leaf_pointer_tensors(groups, dev)
 
 
 class SGDTreeFn(torch.autograd.Function):
@@ -245,8 +245,8 @@ class SGDTreeFn(torch.autograd.Function):
         dev = p[0].device
         po = [torch.empty_like(x) for x in p]
         to = [torch.empty_like(x) for x in p] if mom else None
-        _d.sgd_fwd_tree(table, _ptrs_or_none(p, dev), _ptrs_or_none(g, dev), _ptrs_or_none(t, dev), hyper.lr,
-                        hyper.momentum, hyper.nesterov, _ptrs_or_none(po, dev), _ptrs_or_none(to, dev))
+        a = _ptrs((p, g, t, po, to), dev)
+        _d.sgd_fwd_tree(table, a[0], a[1], a[2], hyper.lr, hyper.momentum, hyper.nesterov, a[3], a[4])
         ctx.table, ctx.hyper, ctx.has_trace, ctx.S = table, hyper, has_trace, S
         ctx.shapes, ctx.dtype, ctx.device = [x.shape for x in p], p[0].dtype, dev
         return (*po, *to) if mom else tuple(po)
@@ -264,8 +264,8 @@ class SGDTreeFn(torch.autograd.Function):
             dT = [zero(sh) if c is None else c.contiguous() for c, sh in zip(cots[S:2 * S], ctx.shapes)]
         dg = [new(sh) for sh in ctx.shapes]
         dt = [new(sh) for sh in ctx.shapes] if mom else None
-        _d.sgd_bwd_tree(ctx.table, _ptrs_or_none(dP, dev), _ptrs_or_none(dT, dev), h.lr, h.momentum, h.nesterov,
-                        _ptrs_or_none(dg, dev), _ptrs_or_none(dt, dev))
+        a = _ptrs((dP, dT, dg, dt), dev)
+        _d.sgd_bwd_tree(ctx.table, a[0], a[1], h.lr, h.momentum, h.nesterov, a[2], a[3])
         # the params path is the identity: the cotangent of each p leaf is dP
         grads = [*dP, *dg]
         if ctx.has_trace:
@@ -292,9 +292,9 @@ class RMSPropTreeFn(torch.autograd.Function):
         vo = [torch.empty_like(x) for x in v]
         bo = [torch.empty_like(x) for x in p] if mom else None
         h = hyper
-        _d.rmsprop_fwd_tree(table, _ptrs_or_none(p, dev), _ptrs_or_none(g, dev), _ptrs_or_none(v, dev),
-                            _ptrs_or_none(b, dev), h.lr, h.alpha, h.eps, h.eps_root, h.momentum,
-                            _ptrs_or_none(po, dev), _ptrs_or_none(vo, dev), _ptrs_or_none(bo, dev))
+        a = _ptrs((p, g, v, b, po, vo, bo), dev)
+        _d.rmsprop_fwd_tree(table, a[0], a[1], a[2], a[3], h.lr, h.alpha, h.eps, h.eps_root, h.momentum, a[4], a[5],
+                            a[6])
         ctx.save_for_backward(*g, *v)
         ctx.table, ctx.hyper, ctx.has_mom, ctx.S = table, hyper, has_mom, S
         return (*po, *vo, *bo) if mom else (*po, *vo)
@@ -318,10 +318,9 @@ class RMSPropTreeFn(torch.autograd.Function):
         dg = [torch.empty_like(x) for x in g]
         dv = [torch.empty_like(x) for x in v]
         db = [torch.empty_like(x) for x in g] if mom else None
-        _d.rmsprop_bwd_tree(ctx.table, _ptrs_or_none(dP, dev), _ptrs_or_none(dV, dev), _ptrs_or_none(dB, dev),
-                            _ptrs_or_none(list(g), dev), _ptrs_or_none(list(v), dev), h.lr, h.alpha, h.eps,
-                            h.eps_root, h.momentum, _ptrs_or_none(dg, dev), _ptrs_or_none(dv, dev),
-                            _ptrs_or_none(db, dev))
+        a = _ptrs((dP, dV, dB, g, v, dg, dv, db), dev)
+        _d.rmsprop_bwd_tree(ctx.table, a[0], a[1], a[2], a[3], a[4], h.lr, h.alpha, h.eps, h.eps_root, h.momentum,
+                            a[5], a[6], a[7])
         grads = [*dP, *dg, *dv]
         if ctx.has_mom:
             grads += db if mom else [None] * S

@@ -277,7 +277,7 @@ def adam_unrolled_bwd(dpK, grads, mu_traj, nu_traj, dgrads, dmu0, dnu0, count0, 
 
 
 # ---- leaf-direct ("tree map") form: every operand is a device int64 tensor of
-# leaf addresses in table order (see tree.leaf_pointer_tensor)
+# leaf addresses in table order (see tree.leaf_pointer_tensors)
 
 
 def _leaf_array(x, what, nseg):

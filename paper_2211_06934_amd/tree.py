@@ -124,19 +124,45 @@ def _stream_context(stream):
     return torch.cuda.stream(stream)
 
 
-def leaf_pointer_tensor(leaves: Sequence[torch.Tensor], device, stream=None) -> torch.Tensor:
-    """Device int64 array of leaf addresses, in table order.
+def leaf_pointer_tensors(groups: Sequence[Optional[Sequence[torch.Tensor]]], device,
+                         stream=None) -> List[Optional[torch.Tensor]]:
+    """One device int64 array of leaf addresses (table order) per group of
+    leaves; None for a group that is None.
 
-    It is allocated on `stream` (default: the current one), the stream whose
-    kernel reads it: torch's caching allocator hands a freed block only to
-    later work on the stream it was allocated on, so the array may be dropped
-    as soon as the kernel is enqueued."""
-    for i, x in enumerate(leaves):
-        if not x.is_contiguous():
-            raise ValueError("leaf %d is not contiguous" % i)
-    ptrs = [x.data_ptr() for x in leaves]
+    All arrays are slices of one device buffer, filled by a single
+    asynchronous copy from pinned host memory, so building them neither waits
+    for the device nor costs one transfer per operand.  The buffer is
+    allocated on `stream` (default: the current one), the stream whose kernels
+    read it: torch's caching allocator hands a freed block only to later work
+    on the stream it was allocated on, so the arrays may be dropped as soon as
+    the kernels are enqueued (the pinned staging block is likewise held until
+    the copy has run)."""
+    ptrs: List[int] = []
+    for g in groups:
+        if g is None:
+            continue
+        for i, x in enumerate(g):
+            if not x.is_contiguous():
+                raise ValueError("leaf %d is not contiguous" % i)
+            ptrs.append(x.data_ptr())
     with _stream_context(stream):
-        return torch.tensor(ptrs, dtype=torch.int64).to(device, non_blocking=False)
+        host = torch.tensor(ptrs, dtype=torch.int64).pin_memory()
+        dev = host.to(device, non_blocking=True)
+    out: List[Optional[torch.Tensor]] = []
+    o = 0
+    for g in groups:
+        if g is None:
+            out.append(None)
+            continue
+        out.append(dev[o:o + len(g)])
+        o += len(g)
+    return out
+
+
+def leaf_pointer_tensor(leaves: Sequence[torch.Tensor], device, stream=None) -> torch.Tensor:
+    """Device int64 array of leaf addresses, in table order (one group of
+    leaf_pointer_tensors)."""
+    return leaf_pointer_tensors([leaves], device, stream)[0]
 
 
 def flatten(tree, out: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, FlatSpec]:
