@@ -107,7 +107,7 @@ def parse():
     ap.add_argument("--workload", default="many_small",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
                              "many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
-                             "es_resnet18"])
+                             "es_resnet18", "adam_vs_torch"])
     ap.add_argument("--trajectory", choices=["stored", "recompute"], default="recompute",
                     help="K-step driver: store every moment state for the backward, or store only the final one "
                          "(and every %d-th) and let the backward recompute the rest in registers" % REMAT_SPAN)
@@ -293,6 +293,58 @@ def phases_treemap(S):
     bl, bb = bwd_plan(K, S["stored"], TREE_UNROLL_CHUNK)
     return [("adam_fwd_tree", "adam_unrolled_fwd_tree", fl, fb * n),
             ("adam_bwd_tree", "adam_unrolled_bwd_tree", bl, bb * n)]
+
+
+VS_TORCH_SIZES = (10 ** 4, 10 ** 5, 10 ** 6, 10 ** 7, 10 ** 8)
+
+
+def torch_op_by_op_sweep(torch, P, sizes, reps):
+    """The paper's accelerated-optimizer comparison (Sec. 2.3, Fig. "results"
+    (a)/(b)) on this GPU: one interior Adam fwd + VJP (count 100, all three
+    cotangents) through the fused kernels against the same step built from
+    torch's own ops (torch.optim's functional Adam in differentiable mode,
+    then autograd), at each size.  Times are HIP-event averages per step."""
+    from torch.optim.adam import adam as torch_adam
+    from workloads import HYPER, torch_normal
+    lr, b1, b2, eps = HYPER["lr"], HYPER["b1"], HYPER["b2"], HYPER["eps"]
+    rows = []
+    for n in sizes:
+        r = lambda seed, std=1.0: torch_normal(n, std, seed, "cuda")  # noqa: E731
+        p, g = r(501, 0.05), r(502, 1e-3)
+        m, v = r(503, 1e-4).abs_(), r(504, 1e-4).abs_()
+        dP, dM, dV = r(505), r(506), r(507)
+        po, mo, vo, dg, dm, dv = (torch.empty(n, device="cuda") for _ in range(6))
+        step_t = torch.tensor(100.0)
+
+        def fused():
+            P.adam_fwd(p, g, m, v, 100, lr, b1, b2, eps, 0.0, po, mo, vo)
+            P.adam_bwd(dP, dM, dV, g, m, v, 100, lr, b1, b2, eps, 0.0, None, dg, dm, dv)
+
+        def op_by_op():
+            pp, gg, mm, vv = (x.detach().requires_grad_() for x in (p, g, m, v))
+            ps, ms, vs = [pp.clone()], [mm.clone()], [vv.clone()]
+            torch_adam(ps, [gg], ms, vs, [], [step_t.clone()], foreach=False, differentiable=True, amsgrad=False,
+                       beta1=b1, beta2=b2, lr=lr, weight_decay=0.0, eps=eps, maximize=False)
+            out = (ps[0] * dP).sum() + (ms[0] * dM).sum() + (vs[0] * dV).sum()
+            torch.autograd.grad(out, [pp, gg, mm, vv])
+
+        times = []
+        for fn in (fused, op_by_op):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0.record()
+            for _ in range(reps):
+                fn()
+            t1.record()
+            torch.cuda.synchronize()
+            times.append(t0.elapsed_time(t1) / reps)
+        rows.append({"n": n, "fused_ms": round(times[0], 4), "torch_op_by_op_ms": round(times[1], 4),
+                     "speedup": round(times[1] / times[0], 2)})
+        del p, g, m, v, dP, dM, dV, po, mo, vo, dg, dm, dv
+        torch.cuda.empty_cache()
+    return rows
 
 
 def setup_flat_1b(torch, P, w):
@@ -567,16 +619,20 @@ def main():
     if not torch.cuda.is_available():
         sys.stderr.write("bench.py: no GPU visible\n")
         sys.exit(1)
-    w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
-                   "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
-                   "es_resnet18": "resnet18_k1"}.get(a.workload, a.workload)]()
+    if a.workload == "adam_vs_torch":
+        from workloads import flat_1b
+        w = flat_1b(VS_TORCH_SIZES[-1])
+    else:
+        w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
+                       "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
+                       "es_resnet18": "resnet18_k1"}.get(a.workload, a.workload)]()
     if a.workload == "es_resnet18":
         S, step, phases = setup_es(torch, P, w), step_es, phases_es
     elif a.workload in ("sgd_treemap", "rmsprop_treemap"):
         S, step, phases = setup_optim_tree(torch, P, a.workload.split("_")[0], w), step_optim_tree, phases_optim_tree
     elif a.workload in ("sgd_flat", "rmsprop_flat"):
         S, step, phases = setup_optim(torch, P, a.workload.split("_")[0]), step_optim, phases_optim
-    elif a.workload == "flat_1b":
+    elif a.workload in ("flat_1b", "adam_vs_torch"):
         S, step, phases = setup_flat_1b(torch, P, w), step_flat_1b, phases_flat_1b
     elif a.workload == "many_small_treemap":
         S, step, phases = setup_treemap(torch, P, w, a.trajectory), step_treemap, phases_treemap
@@ -652,7 +708,7 @@ def main():
 
     cpu = None
     if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap",
-                                                    "rmsprop_treemap", "es_resnet18"):
+                                                    "rmsprop_treemap", "es_resnet18", "adam_vs_torch"):
         cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
         cpu["value"] = float("%.4g" % cpu["value"])
 
@@ -674,6 +730,9 @@ def main():
                    }.get(a.workload, w.description),
                    "n_params": n, "leaves": w.nseg, "K": K,
                    "step": {"flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",
+                            "adam_vs_torch": "one Adam fwd + one Adam bwd (count 100, all cotangents); the same step "
+                                             "through torch's differentiable functional Adam and autograd, timed "
+                                             "beside it over a size sweep",
                             "many_small_treemap": "leaf-direct K-step Adam fwd -> K-step Adam bwd (no flatten)",
                             "sgd_flat": "one SGD fwd + one SGD bwd on the flat buffer",
                             "rmsprop_flat": "one RMSProp fwd + one RMSProp bwd on the flat buffer",
@@ -694,6 +753,8 @@ def main():
         "roofline": roofline, "cpu_baseline": cpu,
         "kernel_src_sha": kernel_source_sha(),
     }
+    if a.workload == "adam_vs_torch":
+        out["vs_torch_op_by_op"] = torch_op_by_op_sweep(torch, P, VS_TORCH_SIZES, max(a.steps, 10))
     print(json.dumps(out), flush=True)
 
 
