@@ -111,8 +111,16 @@ def _addr(x, what: str, dtype=torch.float32, n: Optional[int] = None) -> Optiona
     return x.data_ptr()
 
 
+# torch's current raw stream without building a Stream object (the public
+# torch.cuda.current_stream() costs about as much as a kernel launch)
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_cur_device = getattr(torch._C, "_cuda_getDevice", None)
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
+        if _raw_stream is not None and _cur_device is not None:
+            return _raw_stream(_cur_device())
         return torch.cuda.current_stream().cuda_stream
     if isinstance(stream, int):
         return stream

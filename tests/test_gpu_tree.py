@@ -241,3 +241,15 @@ def test_batched_copies_bit_exact(eb, ntrees):
     with pytest.raises(ValueError):
         P.tree_unflatten_batch(table, flats[:1], [])
     table.close()
+
+
+def test_binding_enqueues_on_the_current_stream():
+    # the binding reads torch's current stream through the raw accessor; it
+    # must be the stream torch itself reports, also inside a stream context
+    import paper_2211_06934_amd as P
+    d = P.diffopt
+    assert d._stream(None) == torch.cuda.current_stream().cuda_stream
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        assert d._stream(None) == side.cuda_stream == torch.cuda.current_stream().cuda_stream
+    assert d._stream(None) == torch.cuda.current_stream().cuda_stream
