@@ -180,3 +180,12 @@ def test_workload_shapes():
     s = many_small_sizes()
     assert len(s) == 20000 and min(s) >= 1 and max(s) <= 65536
     assert 1.0e8 < sum(s) < 1.4e8
+
+
+def test_header_is_plain_c_and_cpp():
+    # the boundary is a C ABI: the header must compile as strict C99 and as C++
+    for cmd in (["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only", "-x", "c", HEADER],
+                ["g++", "-std=c++11", "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only", "-x", "c++",
+                 HEADER]):
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
