@@ -296,6 +296,7 @@ def phases_treemap(S):
 
 
 VS_TORCH_SIZES = (10 ** 4, 10 ** 5, 10 ** 6, 10 ** 7, 10 ** 8)
+COPY_REPS = 5  # timed repetitions of the 1 GiB device-to-device calibration copy
 
 
 def torch_op_by_op_sweep(torch, P, sizes, reps):
@@ -643,11 +644,19 @@ def main():
     torch.cuda.synchronize()
 
     # a plain copy of known size, outside the timed region: the calibration
-    # point for the HBM byte counters of profiling runs of this same command
+    # point for the HBM byte counters of profiling runs of this same command,
+    # and a same-harness device-to-device copy rate to compare against
     cal_src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     cal_dst = torch.empty_like(cal_src)
     cal_dst.copy_(cal_src)
     torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(COPY_REPS):
+        cal_dst.copy_(cal_src)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 2 * cal_src.numel() * 4 * COPY_REPS / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del cal_src, cal_dst
 
     for _ in range(a.warmup):
@@ -695,6 +704,8 @@ def main():
             breakdown[name] = {"ms": round(t, 4), "launches": launches,
                                "GB/s": round(byts / (t * 1e-3) / 1e9, 1),
                                "frac": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            if "fwd" in name or "bwd" in name:  # parameter-steps per second of this phase alone
+                breakdown[name]["G_params_per_s"] = round(n * K / (t * 1e-3) / 1e9, 2)
         dom = max(range(nph), key=lambda i: phase_ms[i])
         dname, dkern, dlaunch, dbytes = ph[dom]
         avg_launch_s = phase_ms[dom] * 1e-3 / dlaunch
@@ -749,6 +760,7 @@ def main():
                       if "stored" in S else {})},
         "us_per_step": round(ms_step * 1e3, 2),
         "achieved_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "d2d_copy_GBps": round(copy_gbs, 1), "frac_of_d2d_copy": round(gbs / copy_gbs, 4),
         "bytes_per_step": int(bytes_step), "phases": breakdown,
         "roofline": roofline, "cpu_baseline": cpu,
         "kernel_src_sha": kernel_source_sha(),
