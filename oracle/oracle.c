@@ -53,6 +53,12 @@
  *   pack    : numpy concatenation, bit for bit; unpack(pack(x)) == x.
  *   mag_*   : the tolerance scales are sums of absolute values of terms and
  *             are checked to bound |value| (triangle inequality).
+ *
+ * Accuracy limit of the plain chain rule: the update's two dg terms (and
+ * RMSProp's) are each of size lr a / s and cancel exactly when the state is
+ * fresh and eps = eps_root = 0, so with a tiny s their fp64 difference keeps
+ * a rounding residue of about 1e-16 lr a / s instead of 0.  Tests in that
+ * regime take dg from the closed form (the update is constant in g there).
  */
 #include <math.h>
 #include <stddef.h>

@@ -227,19 +227,23 @@ __device__ __forceinline__ BwdOut bwd_elem(float dP, float dM, float dV, float g
   const float d = s + c.eps;
   const float N = fmaf(c.bb1_c1 * g, m, -fmaf(c.ab2_c2, v, c.a * fmaf(s, c.eps, c.eps_root)));
   float kg, kvv, km;  // dupdate coefficients of dg, dv and dm
+  // The quotients x / (s d^2) are taken as ((x / s) / d) / d.  N / s stays
+  // in range (each term of N carries g, v, eps_root or s, and s^2 = b2 v/c2 +
+  // b g^2 + eps_root), so when s d^2 itself underflows (tiny s with eps = 0)
+  // the result is still the finite quotient, and an exactly zero N gives 0
+  // rather than 0 * inf.
 #if DIFFOPT_FAST_RECIP
   // two reciprocals, 1/d and 1/s, serve all three quotients; the s == 0
   // case (the explicit 0/0 one, below) is a select, not a branch
   const float rd = __builtin_amdgcn_rcpf(d);
-  const float r = (rd * __builtin_amdgcn_rcpf(s)) * rd;  // 1 / (s d^2)
-  kg = s > 0.0f ? c.lr * N * r : -c.lr_a * rd;
-  kvv = s > 0.0f ? c.kv * m1 * r : 0.0f;
+  const float rs = __builtin_amdgcn_rcpf(s);
+  kg = s > 0.0f ? c.lr * (((N * rs) * rd) * rd) : -c.lr_a * rd;
+  kvv = s > 0.0f ? c.kv * (((m1 * rs) * rd) * rd) : 0.0f;
   km = c.b1_lr_c1 * rd;
 #else
   if (s > 0.0f) {
-    const float sd2 = s * d * d;
-    kg = c.lr * N / sd2;
-    kvv = c.kv * m1 / sd2;
+    kg = c.lr * (((N / s) / d) / d);
+    kvv = c.kv * (((m1 / s) / d) / d);
   } else {
     // s == 0 needs eps_root == 0, v == 0, g == 0: the explicit 0/0 case.
     kg = -c.lr_a / d;

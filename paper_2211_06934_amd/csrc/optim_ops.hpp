@@ -108,9 +108,11 @@ struct RmsBwd {
     const float d = s + c.eps;
     float kg, kv;  // Bt coefficients of dg and of dL/dv'
     if (s > 0.0f) {
-      const float sd2 = s * d * d;
-      kg = fmaf(c.alpha, v, fmaf(s, c.eps, c.eps_root)) / sd2;
-      kv = -g / (2.0f * sd2);
+      // x / (s d^2) as ((x / s) / d) / d: x / s stays in range (s^2 >= alpha v
+      // + eps_root and s >= sqrt(1 - alpha) |g|), so an underflowing s d^2
+      // (tiny s with eps = 0) still gives the finite quotient
+      kg = ((fmaf(c.alpha, v, fmaf(s, c.eps, c.eps_root)) / s) / d) / d;
+      kv = -0.5f * (((g / s) / d) / d);
     } else {
       kg = 1.0f / d;
       kv = 0.0f;

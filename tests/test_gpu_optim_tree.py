@@ -18,7 +18,7 @@ import torch.nn.functional as F
 
 import oracle
 from tests.support import BWD_RTOL, FWD_RTOL, assert_mag_close
-from tests.test_gpu_maml import ConvNet, _normrel, _task
+from tests.test_gpu_maml import ConvNet, _normrel, _task, torch32_spread
 from tests.test_gpu_treemap import _device_tree, _empty_like_tree, _ptrs, _split
 from workloads import abs_normal, normal, random_shapes
 
@@ -227,7 +227,9 @@ def test_maml_meta_gradient_through_fused_sgd_rmsprop(which, hyper, K):
     ref32, _ = _meta_grad_reference(which, init, task, K, "cuda", torch.float32, hyper)
     assert all(torch.isfinite(g).all() for g in ours + ref64 + ref32)
     assert abs(out_ours - out64) <= 1e-4 * abs(out64), (out_ours, out64)
-    e64, t64 = _normrel(ours, ref64), _normrel(ref32, ref64)
-    print("%s K=%d  |ours-fp64|=%.2e  |torch32-fp64|=%.2e" % (which, K, e64, t64))
-    # as for Adam: no further from the fp64 loop than torch's own fp32 loop
+    e64 = _normrel(ours, ref64)
+    t64 = torch32_spread(lambda: _meta_grad_reference(which, init, task, K, "cuda", torch.float32, hyper)[0], ref64)
+    print("%s K=%d  |ours-fp64|=%.2e  max |torch32-fp64|=%.2e" % (which, K, e64, t64))
+    # as for Adam: no further from the fp64 loop than twice the farthest of
+    # three runs of torch's own fp32 loop
     assert e64 < 2 * t64 + 1e-5, (e64, t64)
