@@ -291,7 +291,7 @@ def sgd_fwd_mag(p, g, t, lr, momentum=0.0, nesterov=False):
     p, g = _f64(p), _f64(g)
     at = np.zeros_like(p) if t is None else np.abs(_f64(t, p.size))
     mag_t = momentum * at + np.abs(g)
-    mag_u = lr * (np.abs(g) + momentum * mag_t) if nesterov else lr * mag_t
+    mag_u = abs(lr) * (np.abs(g) + momentum * mag_t) if nesterov else abs(lr) * mag_t
     return np.abs(p) + mag_u, mag_t
 
 
@@ -299,8 +299,8 @@ def sgd_bwd_mag(dP, dT, lr, momentum=0.0, nesterov=False):
     """Tolerance scales (mag_dg, mag_dt) of sgd_bwd: sums of |terms|."""
     dP = np.abs(_f64(dP))
     adT = np.zeros_like(dP) if dT is None else np.abs(_f64(dT, dP.size))
-    mag_T = adT + (lr * momentum if nesterov else lr) * dP
-    mag_dg = mag_T + (lr * dP if nesterov else 0.0)
+    mag_T = adT + abs(lr * momentum if nesterov else lr) * dP
+    mag_dg = mag_T + (abs(lr) * dP if nesterov else 0.0)
     return mag_dg, momentum * mag_T
 
 

@@ -165,7 +165,7 @@ void oracle_adam_fwd_mag(int64_t n, const double* p, const double* g,
     double d = s + eps;
     double am = b1 * fabs(m[i]) + (1.0 - b1) * fabs(g[i]);
     double av = b2 * fabs(v[i]) + (1.0 - b2) * g[i] * g[i];
-    double au = lr * am / (c1 * d);
+    double au = fabs(lr) * am / (c1 * d);
     mag_m[i] = am;
     mag_v[i] = av;
     mag_u[i] = au;
@@ -209,14 +209,14 @@ void oracle_adam_bwd_mag(int64_t n, const double* dP, const double* dM,
     if (s > 0.0) {
       double num = b * b1 * fabs(g[i] * m[i]) / c1 + a * b2 * fabs(v[i]) / c2 +
                    a * (eps_root + s * eps);
-      t3 = adP * lr * num / (s * d * d);
-      tv = adP * lr * amh / (2.0 * c2 * s * d * d);
+      t3 = adP * fabs(lr) * num / (s * d * d);
+      tv = adP * fabs(lr) * amh / (2.0 * c2 * s * d * d);
     } else {
-      t3 = adP * lr * a / d;
+      t3 = adP * fabs(lr) * a / d;
       tv = 0.0;
     }
     mag_dg[i] = (1.0 - b1) * adM + 2.0 * (1.0 - b2) * fabs(g[i]) * adV + t3;
-    mag_dm[i] = b1 * (adM + adP * lr / (c1 * d));
+    mag_dm[i] = b1 * (adM + adP * fabs(lr) / (c1 * d));
     mag_dv[i] = b2 * (adV + tv);
   }
 }
@@ -405,7 +405,7 @@ void oracle_rmsprop_fwd_mag(int64_t n, const double* p, const double* g, const d
     double ab = mu > 0.0 ? mu * fabs(b ? b[i] : 0.0) + aq : aq;
     mag_v[i] = v1;
     if (mag_b) mag_b[i] = ab;
-    mag_p[i] = fabs(p[i]) + lr * ab;
+    mag_p[i] = fabs(p[i]) + fabs(lr) * ab;
   }
 }
 
@@ -415,7 +415,7 @@ void oracle_rmsprop_bwd_mag(int64_t n, const double* dP, const double* dV, const
   for (int64_t i = 0; i < n; ++i) {
     double s = sqrt(alpha * v[i] + (1.0 - alpha) * g[i] * g[i] + eps_root);
     double d = s + eps;
-    double aBt = (mu > 0.0 ? fabs(dB ? dB[i] : 0.0) : 0.0) + lr * fabs(dP[i]);
+    double aBt = (mu > 0.0 ? fabs(dB ? dB[i] : 0.0) : 0.0) + fabs(lr) * fabs(dP[i]);
     double adV = dV ? fabs(dV[i]) : 0.0;
     double t3 = s > 0.0 ? aBt * (alpha * fabs(v[i]) + eps_root + s * eps) / (s * d * d) : aBt / d;
     double tv = s > 0.0 ? aBt * fabs(g[i]) / (2.0 * s * d * d) : 0.0;

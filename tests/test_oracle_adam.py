@@ -270,17 +270,17 @@ def test_mag_bounds_values():
     # The tolerance scales are sums of |terms|, so they bound |value| for every
     # element (triangle inequality); a dropped term usually breaks this.
     n = 5000
-    for count, eps_root in ((0, 0.0), (7, 1e-8), (100, 0.0)):
+    for count, eps_root, lr in ((0, 0.0, LR), (7, 1e-8, LR), (100, 0.0, LR), (7, 1e-8, -LR)):
         p = normal(n, 0.05, "mag", "p0", count).astype(np.float64)
         g = normal(n, 0.01, "mag", "grad", count).astype(np.float64)
         m = normal(n, 1e-3, "mag", "mu", count).astype(np.float64) if count else np.zeros(n)
         v = abs_normal(n, 1e-4, "mag", "nu", count).astype(np.float64) if count else np.zeros(n)
         cots = [normal(n, 1.0, "mag", t, count).astype(np.float64) for t in ("cot_p", "cot_m", "cot_v")]
-        f = oracle.adam_fwd(p, g, m, v, count, LR, B1, B2, EPS, eps_root)
-        fm = oracle.adam_fwd_mag(p, g, m, v, count, LR, B1, B2, EPS, eps_root)
+        f = oracle.adam_fwd(p, g, m, v, count, lr, B1, B2, EPS, eps_root)
+        fm = oracle.adam_fwd_mag(p, g, m, v, count, lr, B1, B2, EPS, eps_root)
         for val, mg in zip(f, fm):
             assert np.all(np.abs(val) <= mg * (1 + 1e-12))
-        b = oracle.adam_bwd(*cots, g, m, v, count, LR, B1, B2, EPS, eps_root)
-        bm = oracle.adam_bwd_mag(*cots, g, m, v, count, LR, B1, B2, EPS, eps_root)
+        b = oracle.adam_bwd(*cots, g, m, v, count, lr, B1, B2, EPS, eps_root)
+        bm = oracle.adam_bwd_mag(*cots, g, m, v, count, lr, B1, B2, EPS, eps_root)
         for val, mg in zip(b[1:], bm):
             assert np.all(np.abs(val) <= mg * (1 + 1e-9))

@@ -197,17 +197,38 @@ def test_rmsprop_zero_over_zero_is_symmetric_derivative():
 
 def test_rmsprop_mag_bounds_values():
     n = 4000
-    for momentum, eps_root in ((0.0, 0.0), (0.9, 1e-8)):
+    for momentum, eps_root, lr in ((0.0, 0.0, 1e-3), (0.9, 1e-8, 1e-3), (0.9, 1e-8, -1e-3)):
         p = normal(n, 0.05, "rmag", "p0").astype(np.float64)
         g = normal(n, 0.01, "rmag", "grad").astype(np.float64)
         v = abs_normal(n, 1e-4, "rmag", "nu").astype(np.float64)
         b = normal(n, 0.1, "rmag", "mu").astype(np.float64)
         cots = [normal(n, 1.0, "rmag", t).astype(np.float64) for t in ("cot_p", "cot_v", "cot_m")]
-        f = oracle.rmsprop_fwd(p, g, v, b, 1e-3, ALPHA, EPS, eps_root, momentum)
-        fm = oracle.rmsprop_fwd_mag(p, g, v, b, 1e-3, ALPHA, EPS, eps_root, momentum)
+        f = oracle.rmsprop_fwd(p, g, v, b, lr, ALPHA, EPS, eps_root, momentum)
+        fm = oracle.rmsprop_fwd_mag(p, g, v, b, lr, ALPHA, EPS, eps_root, momentum)
         for val, mg in zip(f, fm):
             assert np.all(np.abs(val) <= mg * (1 + 1e-12))
-        bw = oracle.rmsprop_bwd(*cots, g, v, 1e-3, ALPHA, EPS, eps_root, momentum)
-        bm = oracle.rmsprop_bwd_mag(*cots, g, v, 1e-3, ALPHA, EPS, eps_root, momentum)
+        bw = oracle.rmsprop_bwd(*cots, g, v, lr, ALPHA, EPS, eps_root, momentum)
+        bm = oracle.rmsprop_bwd_mag(*cots, g, v, lr, ALPHA, EPS, eps_root, momentum)
         for val, mg in zip(bw[1:], bm):
             assert np.all(np.abs(val) <= mg * (1 + 1e-9))
+
+
+def test_sgd_mag_bounds_values():
+    # sums of |terms| bound |value| element by element (triangle inequality),
+    # for either sign of the learning rate
+    n = 4000
+    for momentum, nesterov, lr in ((0.0, False, 0.1), (0.9, False, 0.05), (0.9, True, 0.05), (0.9, True, -0.05)):
+        p = normal(n, 0.05, "smag", "p0").astype(np.float64)
+        g = normal(n, 0.01, "smag", "grad").astype(np.float64)
+        t = normal(n, 0.01, "smag", "mu").astype(np.float64)
+        dP, dT = (normal(n, 1.0, "smag", tag).astype(np.float64) for tag in ("cot_p", "cot_m"))
+        f = oracle.sgd_fwd(p, g, t, lr, momentum, nesterov)
+        fm = oracle.sgd_fwd_mag(p, g, t, lr, momentum, nesterov)
+        for val, mg in zip(f, fm):
+            if momentum == 0.0 and mg is fm[1]:
+                continue  # no trace without momentum
+            assert np.all(np.abs(val) <= mg * (1 + 1e-12))
+        bw = oracle.sgd_bwd(dP, dT, lr, momentum, nesterov)
+        bm = oracle.sgd_bwd_mag(dP, dT, lr, momentum, nesterov)
+        for val, mg in zip(bw[1:], bm):
+            assert np.all(np.abs(val) <= mg * (1 + 1e-12))
