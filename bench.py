@@ -39,6 +39,7 @@ METRIC = "diff-Adam fwd+bwd params/s and achieved HBM GB/s (% of MI355X peak), 1
 # algorithmic bytes per element (fp32): what the method must read + write
 B_FWD = 28          # p, g, m, v -> p', m', v'
 B_BWD = 36          # dP, dM, dV, g, m, v -> dg, dm, dv
+B_BWD_ZERO_MV = 28  # dP, g, m, v -> dg, dm, dv (zero moment cotangents)
 B_BWD_FIRST = 28    # dM = dV = 0: dP, g, m, v -> dg, dm, dv
 B_COPY = 8          # pack / unpack: read once, write once
 UNROLL_CHUNK = 16   # steps per launch of the fused K-step driver
@@ -107,7 +108,7 @@ def parse():
     ap.add_argument("--workload", default="many_small",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
                              "many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
-                             "es_resnet18", "adam_vs_torch"])
+                             "es_resnet18", "adam_vs_torch", "flat_1b_zero_mv"])
     ap.add_argument("--trajectory", choices=["stored", "recompute"], default="recompute",
                     help="K-step driver: store every moment state for the backward, or store only the final one "
                          "(and every %d-th) and let the backward recompute the rest in registers" % REMAT_SPAN)
@@ -348,14 +349,17 @@ def torch_op_by_op_sweep(torch, P, sizes, reps):
     return rows
 
 
-def setup_flat_1b(torch, P, w):
+def setup_flat_1b(torch, P, w, zero_mv=False):
+    """The 10^9-element interior step; zero_mv: the moment cotangents are zero
+    (the first backward step of an unrolled loop), passed as NULL."""
     from workloads import HYPER, torch_normal
     n, dev = w.n, "cuda"
     S = dict(K=1, n=n, hyper=dict(HYPER, eps_root=w.eps_root), count0=w.count0,
              p=torch_normal(n, 0.05, 201, dev), g=torch_normal(n, w.grad_std, 202, dev),
              m=torch_normal(n, 1e-4, 203, dev).abs_(), v=torch_normal(n, 1e-4, 204, dev).abs_(),
-             dP=torch_normal(n, 1.0, 205, dev), dM=torch_normal(n, 1.0, 206, dev),
-             dV=torch_normal(n, 1.0, 207, dev))
+             dP=torch_normal(n, 1.0, 205, dev), zero_mv=zero_mv,
+             dM=None if zero_mv else torch_normal(n, 1.0, 206, dev),
+             dV=None if zero_mv else torch_normal(n, 1.0, 207, dev))
     for k in ("po", "mo", "vo", "dg", "dm", "dv"):
         S[k] = torch.empty(n, dtype=torch.float32, device=dev)
     return S
@@ -505,7 +509,8 @@ def phases_es(S):
 
 def phases_flat_1b(S):
     n = S["n"]
-    return [("adam_fwd", "adam_fwd", 1, B_FWD * n), ("adam_bwd", "adam_bwd", 1, B_BWD * n)]
+    return [("adam_fwd", "adam_fwd", 1, B_FWD * n),
+            ("adam_bwd", "adam_bwd", 1, (B_BWD_ZERO_MV if S.get("zero_mv") else B_BWD) * n)]
 
 
 # ------------------------------------------------------------- CPU baseline
@@ -626,15 +631,15 @@ def main():
     else:
         w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
                        "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
-                       "es_resnet18": "resnet18_k1"}.get(a.workload, a.workload)]()
+                       "es_resnet18": "resnet18_k1", "flat_1b_zero_mv": "flat_1b"}.get(a.workload, a.workload)]()
     if a.workload == "es_resnet18":
         S, step, phases = setup_es(torch, P, w), step_es, phases_es
     elif a.workload in ("sgd_treemap", "rmsprop_treemap"):
         S, step, phases = setup_optim_tree(torch, P, a.workload.split("_")[0], w), step_optim_tree, phases_optim_tree
     elif a.workload in ("sgd_flat", "rmsprop_flat"):
         S, step, phases = setup_optim(torch, P, a.workload.split("_")[0]), step_optim, phases_optim
-    elif a.workload in ("flat_1b", "adam_vs_torch"):
-        S, step, phases = setup_flat_1b(torch, P, w), step_flat_1b, phases_flat_1b
+    elif a.workload in ("flat_1b", "adam_vs_torch", "flat_1b_zero_mv"):
+        S, step, phases = setup_flat_1b(torch, P, w, a.workload == "flat_1b_zero_mv"), step_flat_1b, phases_flat_1b
     elif a.workload == "many_small_treemap":
         S, step, phases = setup_treemap(torch, P, w, a.trajectory), step_treemap, phases_treemap
     else:
@@ -719,7 +724,8 @@ def main():
 
     cpu = None
     if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap",
-                                                    "rmsprop_treemap", "es_resnet18", "adam_vs_torch"):
+                                                    "rmsprop_treemap", "es_resnet18", "adam_vs_torch",
+                                                    "flat_1b_zero_mv"):
         cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
         cpu["value"] = float("%.4g" % cpu["value"])
 
@@ -741,6 +747,8 @@ def main():
                    }.get(a.workload, w.description),
                    "n_params": n, "leaves": w.nseg, "K": K,
                    "step": {"flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",
+                            "flat_1b_zero_mv": "one Adam fwd + one Adam bwd (count 100, zero mu/nu cotangents: "
+                                               "the first backward step of an unrolled loop)",
                             "adam_vs_torch": "one Adam fwd + one Adam bwd (count 100, all cotangents); the same step "
                                              "through torch's differentiable functional Adam and autograd, timed "
                                              "beside it over a size sweep",
