@@ -2,11 +2,14 @@
 
 The product is the HIP library ``libdiffopt.so`` behind ``include/diffopt.h``:
 fused Adam forward, its fused VJP, a K-step unrolled driver, tree
-flatten/unflatten through a segment table, and the leaf-direct ("tree map")
-form of the step that works on the leaves without flattening.  ``diffopt`` is its thin Python
-binding (same entry points), ``tree`` the host-side container walk and
-``autograd`` a torch.autograd.Function over the fused step.  Importing the
-package loads the library and raises ImportError if it has not been built.
+flatten/unflatten through a segment table, the leaf-direct ("tree map") form
+of the step that works on the leaves without flattening, fused differentiable
+SGD-momentum and RMSProp (flat and leaf-direct), and the zero-order (ES)
+estimator.  ``diffopt`` is its thin Python binding (same entry points),
+``tree`` the host-side container walk and ``autograd`` the
+torch.autograd.Functions and meta-optimizers over the fused steps.  Importing
+the package loads the library and raises ImportError if it has not been
+built.
 """
 from . import diffopt
 from .diffopt import (DiffoptError, SegTable, adam_bwd, adam_bwd_tree, adam_fwd, adam_fwd_tree,
@@ -19,7 +22,7 @@ from .diffopt import (DiffoptError, SegTable, adam_bwd, adam_bwd_tree, adam_fwd,
 from . import tree
 from . import autograd
 from .autograd import (AdamFn, AdamHyper, AdamState, AdamTreeFn, FlatAdam, MetaAdam, MetaRMSProp, MetaSGD,
-                       RMSPropHyper, RMSPropTreeFn, SGDHyper, SGDTreeFn)
+                       RMSPropHyper, RMSPropTreeFn, SGDHyper, SGDTreeFn, ZeroOrderFn, es_gradient)
 
 __all__ = [
     "diffopt", "tree", "autograd", "DiffoptError", "SegTable", "adam_bwd", "adam_fwd",
@@ -30,5 +33,5 @@ __all__ = [
     "segtable_nseg", "segtable_total", "tree_flatten", "tree_unflatten", "tree_flatten_batch",
     "tree_unflatten_batch", "AdamFn", "AdamHyper",
     "AdamState", "FlatAdam", "AdamTreeFn", "MetaAdam", "SGDHyper", "SGDTreeFn", "MetaSGD", "RMSPropHyper",
-    "RMSPropTreeFn", "MetaRMSProp",
+    "RMSPropTreeFn", "MetaRMSProp", "ZeroOrderFn", "es_gradient",
 ]
