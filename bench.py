@@ -3,15 +3,25 @@
 One step = one pass of the whole path over one batch of synthetic input:
   tree flatten of the params tree and of K gradient trees (one batched launch)
   -> K-step unrolled Adam forward (the K steps fused in one kernel per 16
-     steps, running params in registers, trajectory kept)
-  -> K-step unrolled Adam backward (the same, running cotangents in registers)
+     steps, running params in registers; by default only the final moment
+     state is stored, --trajectory stored keeps every one)
+  -> K-step unrolled Adam backward (the same, running cotangents in registers,
+     the moments recomputed from the nearest stored state)
   -> tree unflatten of p_K and of the K gradient cotangents (one batched launch).
 Default workload: the many-small-tensor tree (20,000 fp32 leaves, log-uniform
 sizes in [1, 65536], K = 3).  All inputs are resident in HBM before timing.
-Other trees (--workload tiny_mlp | convnet32 | resnet18_k1 | resnet18_k10)
-run the same step; --workload flat_1b times one interior fwd + bwd step on a
-single 10^9-element buffer; --graph replays one captured step as a HIP graph
-(the small trees are launch-bound).
+Other workloads:
+  tiny_mlp | convnet32 | resnet18_k1 | resnet18_k10   the same step on other trees
+  flat_1b [_zero_mv]       one interior fwd + bwd on a 10^9-element buffer
+                           (_zero_mv: zero moment cotangents)
+  many_small_treemap       the K-step pass leaf-direct, without flatten/unflatten
+  sgd_flat | rmsprop_flat | sgd_treemap | rmsprop_treemap
+                           one fwd + bwd of the other fused optimizers
+  es_resnet18              ES perturb + estimate at the ResNet-18 size
+  adam_vs_torch            the interior Adam step at 10^8, plus the same step in
+                           torch ops over a size sweep (field vs_torch_op_by_op)
+--graph replays one captured step as a HIP graph (the small trees are
+launch-bound).
 
 Prints ONE JSON line.  `value` is Adam fwd+bwd parameter-steps per second for
 the whole pass (n * K / step time); `roofline` covers the dominant kernel
