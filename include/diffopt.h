@@ -50,7 +50,8 @@ extern "C" {
  * recomputes from one stored state (see diffopt_adam_unrolled_bwd).        */
 #define DIFFOPT_REMAT_SPAN 8
 
-/* Message describing the last nonzero return on this thread ("" if none).
+/* Message describing the last nonzero return on this thread ("" if none);
+ * error reporting of this ABI, not an operation of the paper.
  * The pointer stays valid until the next diffopt call on the same thread. */
 const char* diffopt_last_error(void);
 
@@ -84,17 +85,21 @@ int diffopt_segtable_create(int64_t nseg, const int64_t* numel,
                             diffopt_segtable** out);
 
 /* Free a table and its device memory (NULL is a no-op).  The caller must
- * make sure no enqueued flatten/unflatten still uses it.                    */
+ * make sure no enqueued flatten/unflatten still uses it.  (The table is the
+ * tree structure of Sec. 2.3 "PyTree", kept on the device.)                 */
 void diffopt_segtable_destroy(diffopt_segtable* table);
 
-/* Flat length n in elements (max over leaves of off_j + numel_j); -1 if
+/* Flat length n in elements of the flattened tree (Sec. 2.3 "PyTree"): the
+ * max over leaves of off_j + numel_j; -1 if
  * table is NULL.                                                            */
 int64_t diffopt_segtable_total(const diffopt_segtable* table);
 
-/* Number of leaves S the table was built for; -1 if table is NULL.          */
+/* Number of leaves S the table was built for (Sec. 2.3 "PyTree"); -1 if
+ * table is NULL.                                                            */
 int64_t diffopt_segtable_nseg(const diffopt_segtable* table);
 
-/* Tree flatten (pack): flat[off_j + i] = leaf_j[i] for all j, i < numel_j.
+/* Tree flatten (pack; Appendix D, Table 2 "Tree Flatten"):
+ * flat[off_j + i] = leaf_j[i] for all j, i < numel_j.
  *   leaf_ptrs   DEVICE array [nseg] of uint64 leaf addresses, in table order
  *               (entries of empty leaves are ignored and may be 0)
  *   flat        device buffer of at least diffopt_segtable_total() elements
@@ -104,7 +109,8 @@ int64_t diffopt_segtable_nseg(const diffopt_segtable* table);
 int diffopt_tree_flatten(const diffopt_segtable* table,
                          const uint64_t* leaf_ptrs, void* flat, void* stream);
 
-/* Tree unflatten (unpack), the mirror: leaf_j[i] = flat[off_j + i].
+/* Tree unflatten (unpack; Appendix D, Table 2 "Tree UnFlatten"), the mirror:
+ * leaf_j[i] = flat[off_j + i].
  * Leaves must not overlap each other or the flat buffer.                     */
 int diffopt_tree_unflatten(const diffopt_segtable* table, const void* flat,
                            const uint64_t* leaf_ptrs, void* stream);
@@ -279,7 +285,8 @@ int diffopt_adam_bwd_tree(const diffopt_segtable* table, const uint64_t* dupdate
                           const uint64_t* dgrad, const uint64_t* dmu_in,
                           const uint64_t* dnu_in, void* stream);
 
-/* K-step unrolled driver in leaf-direct form: the recurrences of
+/* K-step unrolled driver in leaf-direct form (Listing 1's loop; Appendix D,
+ * Table 2 "Tree Map"): the recurrences of
  * diffopt_adam_unrolled_fwd / _bwd with every flat buffer replaced by a tree
  * (a device array of leaf addresses).  grads, mu_traj, nu_traj and dgrads are
  * HOST arrays ([K], [K+1], [K+1], [K]) of such device arrays.  The steps run
@@ -324,7 +331,8 @@ int diffopt_sgd_fwd(const float* params, const float* grad, const float* trace,
                     int64_t n, double lr, double momentum, int32_t nesterov,
                     float* params_out, float* trace_out, void* stream);
 
-/* VJP of diffopt_sgd_fwd.  dparams_out: cotangent of p' (the cotangent of p
+/* VJP of diffopt_sgd_fwd (Sec. 2.3: hand-written backward).  dparams_out:
+ * cotangent of p' (the cotangent of p
  * is the same array); dtrace_out: cotangent of t' (NULL = zero).  Writes the
  * cotangent of g and, when mu > 0, of t (dtrace_in, required then).  The map
  * is linear, so no forward input is needed.                               */
@@ -332,7 +340,8 @@ int diffopt_sgd_bwd(const float* dparams_out, const float* dtrace_out,
                     int64_t n, double lr, double momentum, int32_t nesterov,
                     float* dgrad, float* dtrace_in, void* stream);
 
-/* RMSProp with decay alpha in [0, 1), eps >= 0 outside and eps_root >= 0
+/* RMSProp (Sec. 1, contribution (2)(i)) with decay alpha in [0, 1), eps >= 0
+ * outside and eps_root >= 0
  * inside the root, momentum mu >= 0 (buffer b):
  *   v' = alpha v + (1-alpha) g^2;  d = sqrt(v' + eps_root) + eps
  *   mu == 0: u = -lr g / d          (mom, mom_out ignored)
@@ -344,7 +353,8 @@ int diffopt_rmsprop_fwd(const float* params, const float* grad, const float* nu,
                         float* params_out, float* nu_out, float* mom_out,
                         void* stream);
 
-/* VJP of diffopt_rmsprop_fwd, in the algebraically reduced form (the g^2
+/* VJP of diffopt_rmsprop_fwd (Sec. 2.3: hand-written backward, symbolic
+ * reduction, explicit 0/0 cases), in the algebraically reduced form (the g^2
  * terms of the chain rule cancel).  Cotangents of p', v', b' (dnu_out and
  * dmom_out may be NULL = zero); grad and nu are the forward's INPUTS.
  * Writes the cotangents of g, v and, when mu > 0, of b (dmom_in required).
@@ -410,7 +420,8 @@ int diffopt_es_perturb(const float* params, const float* noise,
                        int64_t num_samples, int64_t n, double sigma,
                        int32_t antithetic, float* out, void* stream);
 
-/* es_estimate: grad_j = scale * sum_i weights_i noise_ij, accumulated in
+/* es_estimate (Sec. 2.2, the Monte-Carlo estimate of the smoothed gradient):
+ * grad_j = scale * sum_i weights_i noise_ij, accumulated in
  * sample order in fp32.  weights is a DEVICE array [num_samples] formed by the
  * caller from its evaluations f_i:
  *   plain:       w_i = f(theta + s z_i),                    scale = 1/(N s)
