@@ -85,8 +85,10 @@ int diffopt_segtable_create(int64_t nseg, const int64_t* numel,
                             diffopt_segtable** out);
 
 /* Free a table and its device memory (NULL is a no-op).  The caller must
- * make sure no enqueued flatten/unflatten still uses it.  (The table is the
- * tree structure of Sec. 2.3 "PyTree", kept on the device.)                 */
+ * make sure no enqueued call still uses it, and must not destroy a table
+ * while a stream is being captured into a graph (freeing device memory is
+ * not a capturable operation).  (The table is the tree structure of
+ * Sec. 2.3 "PyTree", kept on the device.)                                   */
 void diffopt_segtable_destroy(diffopt_segtable* table);
 
 /* Flat length n in elements of the flattened tree (Sec. 2.3 "PyTree"): the

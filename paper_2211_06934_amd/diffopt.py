@@ -135,7 +135,11 @@ def _ptr_array(items, what, n):
 
 
 class SegTable:
-    """Owner of a diffopt_segtable handle (freed on close() or collection)."""
+    """Owner of a diffopt_segtable handle (freed on close() or collection).
+
+    Keep it alive while calls that use it may still run, and outside graph
+    capture: freeing its device memory is not a capturable operation.  The
+    tree module caches one table per structure for the life of the process."""
 
     def __init__(self, handle: int, numel: Sequence[int], offsets, elem_bytes: int):
         self.handle = handle
