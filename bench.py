@@ -163,15 +163,18 @@ def kernel_source_sha(kernel=None):
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(kernel, workload):
+def traffic_from_profile(kernel, workload, algorithmic_bytes_per_launch):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel sources; else None."""
+    taken on the current kernel sources and on a launch of the same
+    algorithmic size (the same workload and store policy); else None."""
     path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel, workload))
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
     if rec.get("kernel_src_sha") != kernel_source_sha(kernel):
+        return None
+    if rec.get("algorithmic_bytes_per_launch") != int(algorithmic_bytes_per_launch):
         return None
     return rec.get("bytes_per_launch")
 
@@ -728,7 +731,7 @@ def main():
         achieved = per_launch_bytes / avg_launch_s / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": traffic_from_profile(dkern, a.workload),
+                    "traffic": traffic_from_profile(dkern, a.workload, per_launch_bytes),
                     "kernel": dkern, "bytes_per_launch": int(per_launch_bytes),
                     "avg_launch_us": round(avg_launch_s * 1e6, 2)}
 

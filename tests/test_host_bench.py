@@ -56,3 +56,20 @@ def test_launch_boundaries():
     assert b.bwd_plan(17, st, 16) == (2, (4 + 8 + 16 * 16) + (4 + 8 + 8 + 16))
     # the leaf-direct driver launches every 8 steps
     assert b.fwd_plan(9, b.stored_states(9, "stored"), 8)[0] == 2
+
+
+def test_traffic_record_applies_only_to_its_own_launch_size():
+    # a committed counter record is reported only for the kernel sources and
+    # the per-launch algorithmic bytes it was taken on (a run with another
+    # store policy launches a different amount of work)
+    import glob
+    import json
+    b = _bench()
+    recs = sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.json")))
+    assert recs
+    rec = json.load(open(recs[0]))
+    if rec["kernel_src_sha"] != b.kernel_source_sha(rec["kernel"]):
+        return  # stale record: reported as null anyway
+    alg = rec["algorithmic_bytes_per_launch"]
+    assert b.traffic_from_profile(rec["kernel"], rec["workload"], alg) == rec["bytes_per_launch"]
+    assert b.traffic_from_profile(rec["kernel"], rec["workload"], alg + 4) is None
