@@ -189,3 +189,21 @@ def test_header_is_plain_c_and_cpp():
                  HEADER]):
         r = subprocess.run(cmd, capture_output=True, text=True)
         assert r.returncode == 0, r.stderr
+
+
+def test_tree_walk_edge_structures_on_host():
+    # empty containers and None leaves keep their place; rebuilding with other
+    # leaves gives the same structure; unsupported nodes are refused
+    from paper_2211_06934_amd.tree import tree_build, tree_leaves
+    tree = {"e": [], "t": (), "d": {}, "n": None, "x": [[[torch.ones(2)]], ()], "y": (torch.zeros(0),)}
+    leaves, td = tree_leaves(tree)
+    assert [tuple(x.shape) for x in leaves] == [(2,), (0,)]  # keys sorted: d, e, n, t, x, y
+    back = tree_build(td, [torch.full((2,), 5.0), torch.empty(0)])
+    assert back["e"] == [] and back["t"] == () and back["d"] == {} and back["n"] is None
+    assert torch.equal(back["x"][0][0][0], torch.full((2,), 5.0)) and back["x"][1] == ()
+    assert isinstance(back["y"], tuple) and back["y"][0].numel() == 0
+    assert td.num_leaves == 2
+    with pytest.raises(TypeError):
+        tree_leaves({"a": 3.0})
+    with pytest.raises(TypeError):
+        tree_leaves([torch.ones(1), "s"])
