@@ -253,3 +253,24 @@ def test_binding_enqueues_on_the_current_stream():
     with torch.cuda.stream(side):
         assert d._stream(None) == side.cuda_stream == torch.cuda.current_stream().cuda_stream
     assert d._stream(None) == torch.cuda.current_stream().cuda_stream
+
+
+@pytest.mark.parametrize("dtype", [torch.float16, torch.bfloat16, torch.float64, torch.int8, torch.int64])
+def test_python_tree_api_other_dtypes(dtype):
+    # the table follows the leaves' element size (1, 2, 4 or 8 bytes); the
+    # copies move bits, so every dtype round-trips exactly
+    import paper_2211_06934_amd as P
+    g = torch.Generator(device="cuda").manual_seed(3)
+    shapes = [(3, 5), (7,), (0,), (1,), (33, 3)]
+    if dtype.is_floating_point:
+        leaves = [torch.randn(s, device="cuda", generator=g).to(dtype) for s in shapes]
+    else:
+        leaves = [torch.randint(-100, 100, s, device="cuda", generator=g).to(dtype) for s in shapes]
+    tree = {"w": leaves[:2], "e": leaves[2], "b": tuple(leaves[3:])}
+    flat, spec = P.tree.flatten(tree)
+    order, _ = P.tree.tree_leaves(tree)
+    assert flat.dtype == dtype and flat.numel() == sum(x.numel() for x in leaves)
+    assert torch.equal(flat, torch.cat([x.reshape(-1) for x in order]))
+    back = P.tree.unflatten(flat, spec)
+    for a, b in zip(P.tree.tree_leaves(back)[0], order):
+        assert a.dtype == dtype and a.shape == b.shape and torch.equal(a, b)
