@@ -69,18 +69,21 @@ def test_adamfn_moment_cotangents_flow():
         assert np.all(np.abs(to(got) - r) <= BWD_RTOL * mg)
 
 
-@pytest.mark.parametrize("stored", ["all", "final"])
-def test_unrolled_driver_in_hip_graph_replays(stored):
+@pytest.mark.parametrize("stored,K", [("all", 5), ("final", 5), ((5,), 10), ((7, 15), 17)])
+def test_unrolled_driver_in_hip_graph_replays(stored, K):
     # "final": only the final moment state is stored and the backward
-    # recomputes the trajectory
+    # recomputes the trajectory; K = 10 with state 5 stored runs two recompute
+    # launches; K = 17 with states 7 and 15 stored crosses the forward's 16-step launch
+    # boundary on an unstored state (the running moments pass through the
+    # final-state buffers)
     import paper_2211_06934_amd as P
     w = WORKLOADS["convnet32"]()
-    K, n = w.K, w.n
+    n = w.n
     inp = host_inputs(w)
     dev = "cuda"
     p0 = torch.from_numpy(inp.p0).to(dev)
-    g = [torch.from_numpy(inp.grads[k]).to(dev) for k in range(K)]
-    keep = lambda k: stored == "all" or k == K  # noqa: E731
+    g = [torch.from_numpy(inp.grads[k % w.K]).to(dev) * (1.0 + 0.1 * k) for k in range(K)]
+    keep = lambda k: stored == "all" or k == K or (isinstance(stored, tuple) and k in stored)  # noqa: E731
     mt = [torch.zeros(n, device=dev)] + [torch.empty(n, device=dev) if keep(k) else None for k in range(1, K + 1)]
     vt = [torch.zeros(n, device=dev)] + [torch.empty(n, device=dev) if keep(k) else None for k in range(1, K + 1)]
     pK = torch.empty(n, device=dev)
