@@ -73,3 +73,27 @@ def test_traffic_record_applies_only_to_its_own_launch_size():
     alg = rec["algorithmic_bytes_per_launch"]
     assert b.traffic_from_profile(rec["kernel"], rec["workload"], alg) == rec["bytes_per_launch"]
     assert b.traffic_from_profile(rec["kernel"], rec["workload"], alg + 4) is None
+
+
+def test_documented_paths_exist():
+    # every repository path the design notes and the README name must exist
+    import re
+    for doc in ("DESIGN.md", "README.md"):
+        text = open(os.path.join(ROOT, doc)).read()
+        for path in sorted(set(re.findall(r"`((?:tests|profiles|oracle|include|paper_2211_06934_amd|workloads)/"
+                                          r"[A-Za-z0-9_./{},-]+)`", text))):
+            if "{" in path:  # brace lists such as profiles/kernels_{sgd,rmsprop}_treemap.md
+                head, alts, tail = re.match(r"(.*)\{([^}]*)\}(.*)", path).groups()
+                paths = [head + a + tail for a in alts.split(",")]
+            else:
+                paths = [path]
+            for p in paths:
+                assert os.path.exists(os.path.join(ROOT, p.rstrip("/"))), "%s names missing %s" % (doc, p)
+
+
+def test_kernel_source_lists_name_existing_files():
+    b = _bench()
+    csrc = os.path.join(ROOT, "paper_2211_06934_amd", "csrc")
+    for fam, files in b.KERNEL_SOURCES.items():
+        for f in files:
+            assert os.path.exists(os.path.join(csrc, f)), (fam, f)
