@@ -15,6 +15,8 @@ Other workloads:
   flat_1b [_zero_mv]       one interior fwd + bwd on a 10^9-element buffer
                            (_zero_mv: zero moment cotangents)
   many_small_treemap       the K-step pass leaf-direct, without flatten/unflatten
+  many_small_stepwise      the same pass with one launch per Adam step (the form
+                           a live inner loop needs)
   sgd_flat | rmsprop_flat | sgd_treemap | rmsprop_treemap
                            one fwd + bwd of the other fused optimizers
   es_resnet18              ES perturb + estimate at the ResNet-18 size
@@ -118,7 +120,7 @@ def parse():
     ap.add_argument("--workload", default="many_small",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
                              "many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
-                             "es_resnet18", "adam_vs_torch", "flat_1b_zero_mv"])
+                             "es_resnet18", "adam_vs_torch", "flat_1b_zero_mv", "many_small_stepwise"])
     ap.add_argument("--trajectory", choices=["stored", "recompute"], default="recompute",
                     help="K-step driver: store every moment state for the backward, or store only the final one "
                          "(and every %d-th) and let the backward recompute the rest in registers" % REMAT_SPAN)
@@ -237,6 +239,51 @@ def step_tree(P, S, ev=None):
     P.tree_unflatten_batch(S["table"], [S["pK"]] + S["dg"], [S["pK_ptrs"]] + S["dg_ptrs"])
     if ev:
         ev[4].record()
+
+
+def setup_stepwise(torch, P, w):
+    """The default pass with one launch per Adam step (the form a live inner
+    loop needs, where each gradient depends on the previous step's params):
+    every moment state is stored, and the VJP walks the steps one kernel each."""
+    S = setup_tree(torch, P, w, "stored")
+    S["p_steps"] = [S["p0"]] + [torch.empty_like(S["p0"]) for _ in range(S["K"] - 1)] + [S["pK"]]
+    return S
+
+
+def step_stepwise(P, S, ev=None):
+    h = S["hyper"]
+    K = S["K"]
+    co = [h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"]]
+    if ev:
+        ev[0].record()
+    P.tree_flatten_batch(S["table"], [S["p_ptrs"]] + S["g_ptrs"], [S["p0"]] + S["g"])
+    if ev:
+        ev[1].record()
+    ps, mu, nu = S["p_steps"], S["mu"], S["nu"]
+    for k in range(K):
+        P.adam_fwd(ps[k], S["g"][k], mu[k], nu[k], S["count0"] + k, *co, ps[k + 1], mu[k + 1], nu[k + 1])
+    if ev:
+        ev[2].record()
+    for k in range(K - 1, -1, -1):
+        first = k == K - 1  # zero cotangents of the final moments
+        P.adam_bwd(S["cot"], None if first else S["dm0"], None if first else S["dv0"], S["g"][k], mu[k], nu[k],
+                   S["count0"] + k, *co, None, S["dg"][k], S["dm0"], S["dv0"])
+    if ev:
+        ev[3].record()
+    P.tree_unflatten_batch(S["table"], [S["pK"]] + S["dg"], [S["pK_ptrs"]] + S["dg_ptrs"])
+    if ev:
+        ev[4].record()
+
+
+def phases_stepwise(S):
+    K, n = S["K"], S["n"]
+    cl = -(-(K + 1) // COPY_BATCH)
+    return [
+        ("flatten", "tree_flatten", cl, (K + 1) * B_COPY * n),
+        ("adam_fwd", "adam_fwd", K, K * B_FWD * n),
+        ("adam_bwd", "adam_bwd", K, (K * B_BWD - (B_BWD - B_BWD_ZERO_MV)) * n),
+        ("unflatten", "tree_unflatten", cl, (K + 1) * B_COPY * n),
+    ]
 
 
 def phases_tree(S):
@@ -644,7 +691,8 @@ def main():
     else:
         w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
                        "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
-                       "es_resnet18": "resnet18_k1", "flat_1b_zero_mv": "flat_1b"}.get(a.workload, a.workload)]()
+                       "es_resnet18": "resnet18_k1", "flat_1b_zero_mv": "flat_1b",
+                       "many_small_stepwise": "many_small"}.get(a.workload, a.workload)]()
     if a.workload == "es_resnet18":
         S, step, phases = setup_es(torch, P, w), step_es, phases_es
     elif a.workload in ("sgd_treemap", "rmsprop_treemap"):
@@ -653,6 +701,8 @@ def main():
         S, step, phases = setup_optim(torch, P, a.workload.split("_")[0]), step_optim, phases_optim
     elif a.workload in ("flat_1b", "adam_vs_torch", "flat_1b_zero_mv"):
         S, step, phases = setup_flat_1b(torch, P, w, a.workload == "flat_1b_zero_mv"), step_flat_1b, phases_flat_1b
+    elif a.workload == "many_small_stepwise":
+        S, step, phases = setup_stepwise(torch, P, w), step_stepwise, phases_stepwise
     elif a.workload == "many_small_treemap":
         S, step, phases = setup_treemap(torch, P, w, a.trajectory), step_treemap, phases_treemap
     else:
@@ -738,7 +788,7 @@ def main():
     cpu = None
     if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap",
                                                     "rmsprop_treemap", "es_resnet18", "adam_vs_torch",
-                                                    "flat_1b_zero_mv"):
+                                                    "flat_1b_zero_mv", "many_small_stepwise"):
         cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
         cpu["value"] = float("%.4g" % cpu["value"])
 
@@ -760,6 +810,8 @@ def main():
                    }.get(a.workload, w.description),
                    "n_params": n, "leaves": w.nseg, "K": K,
                    "step": {"flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",
+                            "many_small_stepwise": "flatten p + K grads -> K single-step Adam fwd launches -> K "
+                                                   "single-step Adam bwd launches -> unflatten p_K + K dg",
                             "flat_1b_zero_mv": "one Adam fwd + one Adam bwd (count 100, zero mu/nu cotangents: "
                                                "the first backward step of an unrolled loop)",
                             "adam_vs_torch": "one Adam fwd + one Adam bwd (count 100, all cotangents); the same step "
