@@ -1,6 +1,6 @@
 """The benchmark's own timed steps (every workload it offers but the flat 10^9
-case, which tests/test_gpu_unrolled.py covers in its own launch configuration),
-at full size, against the oracle.
+cases, which tests/test_gpu_unrolled.py covers in their own launch
+configuration, and the torch comparison), at full size, against the oracle.
 
 bench.py's setup and step functions are called as they are (same leaves,
 same batched copies, same store policy and launch plan), and the outputs are
@@ -200,3 +200,33 @@ def test_es_step():
     scale = 1.0 / (2 * N * sigma)
     g = S["grad"].index_select(0, idx).cpu().numpy().astype(np.float64)
     assert_mag_close(g, oracle.es_estimate(Z, w, scale), oracle.es_estimate_mag(Z, w, scale), BWD_RTOL, "estimate")
+
+
+def test_stepwise_pass():
+    # the one-launch-per-step form of the default pass: the same outputs as
+    # the oracle, and bit for bit those of the fused driver on the same inputs
+    import paper_2211_06934_amd as P
+    b = _bench()
+    w = WORKLOADS["many_small"]()
+    S = b.setup_stepwise(torch, P, w)
+    b.step_stepwise(P, S)
+    torch.cuda.synchronize()
+    K = S["K"]
+    p_tree, g_trees, pK_tree, dg_trees = S["keep"]
+    assert torch.equal(S["pK"].view(torch.int32), _cat(pK_tree).view(torch.int32))
+    flat = dict(p0=S["p0"], g=S["g"], cot=S["cot"], pK=S["pK"], muK=S["mu"][K], nuK=S["nu"][K], dg=S["dg"],
+                dm0=S["dm0"], dv0=S["dv0"])
+    _check_adam(S, flat, _sample(S["n"], 200_000, 16))
+    # the fused driver from the same packed inputs
+    e = lambda: torch.empty_like(S["p0"])  # noqa: E731
+    mt = [S["mu"][0]] + [None] * (K - 1) + [e()]
+    vt = [S["nu"][0]] + [None] * (K - 1) + [e()]
+    pK, dg, dm0, dv0 = e(), [e() for _ in range(K)], e(), e()
+    h = S["hyper"]
+    co = (S["count0"], h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+    P.adam_unrolled_fwd(S["p0"], S["g"], mt, vt, pK, *co)
+    P.adam_unrolled_bwd(S["cot"], S["g"], mt, vt, dg, dm0, dv0, *co)
+    torch.cuda.synchronize()
+    pairs = [(pK, S["pK"]), (mt[K], S["mu"][K]), (vt[K], S["nu"][K]), (dm0, S["dm0"]), (dv0, S["dv0"])]
+    for a, c in pairs + list(zip(dg, S["dg"])):
+        assert torch.equal(a.view(torch.int32), c.view(torch.int32))
