@@ -207,3 +207,32 @@ def test_tree_walk_edge_structures_on_host():
         tree_leaves({"a": 3.0})
     with pytest.raises(TypeError):
         tree_leaves([torch.ones(1), "s"])
+
+
+def test_error_messages_are_per_thread():
+    # diffopt_last_error() is thread-local: concurrent failing calls on two
+    # host threads each read back their own message
+    import threading
+    import paper_2211_06934_amd as P
+    lib = P.diffopt._lib
+    f = ctypes.c_void_p(16)  # never dereferenced: both calls fail validation first
+    out = {}
+    barrier = threading.Barrier(2)
+
+    def worker(tag):
+        for _ in range(200):
+            if tag == "count":
+                rc = lib.diffopt_adam_fwd(f, f, f, f, 4, -1, 1e-3, .9, .999, 1e-8, 0., f, f, f, None, None)
+            else:
+                rc = lib.diffopt_adam_fwd(f, f, f, f, 4, 0, 1e-3, 1.5, .999, 1e-8, 0., f, f, f, None, None)
+            barrier.wait()
+            out.setdefault(tag, []).append((rc, P.diffopt.last_error()))
+            barrier.wait()
+
+    ts = [threading.Thread(target=worker, args=(t,)) for t in ("count", "b1")]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert all(rc == -1 and "count" in msg for rc, msg in out["count"])
+    assert all(rc == -1 and "b1" in msg for rc, msg in out["b1"])
