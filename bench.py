@@ -676,7 +676,7 @@ def cpu_baseline_flat_1b(w, target_s):
 def main():
     a = parse()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        sys.stderr.write("bench.py: this build runs on one GPU only; --gpus %d is not supported "
+        sys.stderr.write("bench.py: the benchmark runs on one GPU only; --gpus %d is not supported "
                          "(the kernels are elementwise and would shard by contiguous ranges)\n" % a.gpus)
         sys.exit(2)
     import torch

@@ -2,7 +2,7 @@
  * oracle.c -- plain CPU reference for the differentiable Adam step, its
  * vector-Jacobian product, the K-step unrolled driver and tree pack/unpack.
  *
- * TEST INFRASTRUCTURE ONLY.  This file is the checker the GPU path is judged
+ * TEST INFRASTRUCTURE ONLY.  This file is the oracle the GPU path is tested
  * against.  Only the test-suite, the smoke check and the CPU-baseline leg of
  * the benchmark may load it.  It shares no source, header, table or helper
  * with the HIP library, and the HIP library never calls it.
