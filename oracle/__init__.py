@@ -40,37 +40,47 @@ def _load():
     global _lib
     if _lib is None:
         build()
-        lib = ctypes.CDLL(_LIB)
-        d = ctypes.POINTER(ctypes.c_double)
-        i64 = ctypes.c_int64
-        f64 = ctypes.c_double
-        hyper = [i64, f64, f64, f64, f64, f64]  # count, lr, b1, b2, eps, eps_root
-        lib.oracle_adam_fwd.argtypes = [i64, d, d, d, d, *hyper, d, d, d, d]
-        lib.oracle_adam_bwd.argtypes = [i64, d, d, d, d, d, d, *hyper, d, d, d, d]
-        lib.oracle_adam_fwd_mag.argtypes = [i64, d, d, d, d, *hyper, d, d, d, d]
-        lib.oracle_adam_bwd_mag.argtypes = [i64, d, d, d, d, d, d, *hyper, d, d, d]
-        lib.oracle_unrolled_fwd.argtypes = [i64, i64, d, d, d, d, *hyper, d, d, d]
-        lib.oracle_unrolled_bwd.argtypes = [i64, i64, d, d, d, d, *hyper, d, d, d, d]
-        vp = ctypes.c_void_p
-        lib.oracle_pack.argtypes = [i64, ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
-                                    ctypes.POINTER(vp), vp]
-        lib.oracle_unpack.argtypes = [i64, ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
-                                      vp, ctypes.POINTER(vp)]
-        lib.oracle_sgd_fwd.argtypes = [i64, d, d, d, f64, f64, i64, d, d]
-        lib.oracle_sgd_bwd.argtypes = [i64, d, d, f64, f64, i64, d, d]
-        rms = [f64, f64, f64, f64, f64]  # lr, alpha, eps, eps_root, mu
-        lib.oracle_rmsprop_fwd.argtypes = [i64, d, d, d, d, *rms, d, d, d]
-        lib.oracle_rmsprop_bwd.argtypes = [i64, d, d, d, d, d, *rms, d, d, d]
-        lib.oracle_rmsprop_fwd_mag.argtypes = [i64, d, d, d, d, *rms, d, d, d]
-        lib.oracle_rmsprop_bwd_mag.argtypes = [i64, d, d, d, d, d, *rms, d, d, d]
-        for f in ("oracle_sgd_fwd", "oracle_sgd_bwd", "oracle_rmsprop_fwd", "oracle_rmsprop_bwd",
-                  "oracle_rmsprop_fwd_mag", "oracle_rmsprop_bwd_mag",
-                  "oracle_adam_fwd", "oracle_adam_bwd", "oracle_adam_fwd_mag",
-                  "oracle_adam_bwd_mag", "oracle_unrolled_fwd", "oracle_unrolled_bwd",
-                  "oracle_pack", "oracle_unpack"):
-            getattr(lib, f).restype = None
-        _lib = lib
+        _lib = _configure(ctypes.CDLL(_LIB))
     return _lib
+
+
+def _configure(lib):
+    """Declare the C signatures on a loaded copy of the oracle library (the
+    tests also load deliberately altered builds of it, to show that their
+    pins catch a planted mistake)."""
+    d = ctypes.POINTER(ctypes.c_double)
+    i64 = ctypes.c_int64
+    f64 = ctypes.c_double
+    hyper = [i64, f64, f64, f64, f64, f64]  # count, lr, b1, b2, eps, eps_root
+    lib.oracle_adam_fwd.argtypes = [i64, d, d, d, d, *hyper, d, d, d, d]
+    lib.oracle_adam_bwd.argtypes = [i64, d, d, d, d, d, d, *hyper, d, d, d, d]
+    lib.oracle_adam_fwd_mag.argtypes = [i64, d, d, d, d, *hyper, d, d, d, d]
+    lib.oracle_adam_bwd_mag.argtypes = [i64, d, d, d, d, d, d, *hyper, d, d, d]
+    lib.oracle_unrolled_fwd.argtypes = [i64, i64, d, d, d, d, *hyper, d, d, d]
+    lib.oracle_unrolled_bwd.argtypes = [i64, i64, d, d, d, d, *hyper, d, d, d, d]
+    vp = ctypes.c_void_p
+    lib.oracle_pack.argtypes = [i64, ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
+                                ctypes.POINTER(vp), vp]
+    lib.oracle_unpack.argtypes = [i64, ctypes.POINTER(i64), ctypes.POINTER(i64), i64,
+                                  vp, ctypes.POINTER(vp)]
+    lib.oracle_sgd_fwd.argtypes = [i64, d, d, d, f64, f64, i64, d, d]
+    lib.oracle_sgd_bwd.argtypes = [i64, d, d, f64, f64, i64, d, d]
+    rms = [f64, f64, f64, f64, f64]  # lr, alpha, eps, eps_root, mu
+    lib.oracle_rmsprop_fwd.argtypes = [i64, d, d, d, d, *rms, d, d, d]
+    lib.oracle_rmsprop_bwd.argtypes = [i64, d, d, d, d, d, *rms, d, d, d]
+    lib.oracle_rmsprop_fwd_mag.argtypes = [i64, d, d, d, d, *rms, d, d, d]
+    lib.oracle_rmsprop_bwd_mag.argtypes = [i64, d, d, d, d, d, *rms, d, d, d]
+    for f in ("oracle_sgd_fwd", "oracle_sgd_bwd", "oracle_rmsprop_fwd", "oracle_rmsprop_bwd",
+              "oracle_rmsprop_fwd_mag", "oracle_rmsprop_bwd_mag",
+              "oracle_adam_fwd", "oracle_adam_bwd", "oracle_adam_fwd_mag",
+              "oracle_adam_bwd_mag", "oracle_unrolled_fwd", "oracle_unrolled_bwd",
+              "oracle_pack", "oracle_unpack"):
+        getattr(lib, f).restype = None
+    lib.oracle_es_perturb.argtypes = [i64, i64, d, d, f64, i64, d]
+    lib.oracle_es_perturb.restype = None
+    lib.oracle_es_estimate.argtypes = [i64, i64, d, d, f64, d]
+    lib.oracle_es_estimate.restype = None
+    return lib
 
 
 def _f64(x, n=None):
@@ -311,11 +321,7 @@ def es_perturb(theta, noise, sigma, antithetic=False):
     Z = np.ascontiguousarray(np.asarray(noise, dtype=np.float64).reshape(-1, n))
     N = Z.shape[0]
     out = np.empty(((2 if antithetic else 1) * N, n))
-    lib = _load()
-    lib.oracle_es_perturb.argtypes = [ctypes.c_int64, ctypes.c_int64] + [ctypes.POINTER(ctypes.c_double)] * 2 + \
-        [ctypes.c_double, ctypes.c_int64, ctypes.POINTER(ctypes.c_double)]
-    lib.oracle_es_perturb.restype = None
-    lib.oracle_es_perturb(N, n, _ptr(theta), _ptr(Z), float(sigma), int(bool(antithetic)), _ptr(out))
+    _load().oracle_es_perturb(N, n, _ptr(theta), _ptr(Z), float(sigma), int(bool(antithetic)), _ptr(out))
     return out
 
 
@@ -326,11 +332,7 @@ def es_estimate(noise, weights, scale):
     Z = np.ascontiguousarray(np.asarray(noise, dtype=np.float64).reshape(N, -1))
     n = Z.shape[1]
     g = np.empty(n)
-    lib = _load()
-    lib.oracle_es_estimate.argtypes = [ctypes.c_int64, ctypes.c_int64] + [ctypes.POINTER(ctypes.c_double)] * 2 + \
-        [ctypes.c_double, ctypes.POINTER(ctypes.c_double)]
-    lib.oracle_es_estimate.restype = None
-    lib.oracle_es_estimate(N, n, _ptr(Z), _ptr(w), float(scale), _ptr(g))
+    _load().oracle_es_estimate(N, n, _ptr(Z), _ptr(w), float(scale), _ptr(g))
     return g
 
 

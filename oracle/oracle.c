@@ -51,8 +51,11 @@
  *             exactly 0 since the update vanishes for every v >= 0.
  *   unrolled: fp64 central differences of the K-step map.
  *   pack    : numpy concatenation, bit for bit; unpack(pack(x)) == x.
- *   mag_*   : the tolerance scales are sums of absolute values of terms and
- *             are checked to bound |value| (triangle inequality).
+ *   mag_*   : the tolerance scales are sums of absolute values of terms.
+ *             From below they bound |value| (triangle inequality); from
+ *             above they equal |value| on inputs whose terms all share one
+ *             sign, and copies of this file with any one term doubled are
+ *             built and shown to fail that equality.
  *
  * Accuracy limit of the plain chain rule: the update's two dg terms (and
  * RMSProp's) are each of size lr a / s and cancel exactly when the state is

@@ -5,12 +5,19 @@ Mirrors Listing 1's functional API: ``opt.init`` creates (mu, nu, count);
 one call of AdamFn, whose backward is the library's VJP kernel (Sec. 2.3:
 the optimizer as one operator with a hand-written backward).  The Function
 only allocates outputs and forwards pointers to the C ABI.
+
+Every backward here is a kernel with no autograd graph of its own, so the
+Functions are differentiable once (``once_differentiable``): a first-order
+meta-gradient through any number of unrolled steps works, and asking for a
+higher-order one (``create_graph=True`` through a fused step) raises an error
+instead of silently treating the VJP's inputs as constants.
 """
 from __future__ import annotations
 
 import dataclasses
 
 import torch
+from torch.autograd.function import once_differentiable
 
 from . import diffopt as _d
 
@@ -46,6 +53,7 @@ class AdamFn(torch.autograd.Function):
         return po, mo, vo
 
     @staticmethod
+    @once_differentiable
     def backward(ctx, dP, dM, dV):
         g, m, v = ctx.saved_tensors
         h = ctx.hyper
@@ -106,6 +114,7 @@ class AdamTreeFn(torch.autograd.Function):
         return (*po, *mo, *vo)
 
     @staticmethod
+    @once_differentiable
     def backward(ctx, *cots):
         from .tree import leaf_pointer_tensors
         S, h = ctx.S, ctx.hyper
@@ -252,6 +261,7 @@ class SGDTreeFn(torch.autograd.Function):
         return (*po, *to) if mom else tuple(po)
 
     @staticmethod
+    @once_differentiable
     def backward(ctx, *cots):
         S, h = ctx.S, ctx.hyper
         mom = h.momentum > 0
@@ -300,6 +310,7 @@ class RMSPropTreeFn(torch.autograd.Function):
         return (*po, *vo, *bo) if mom else (*po, *vo)
 
     @staticmethod
+    @once_differentiable
     def backward(ctx, *cots):
         S, h = ctx.S, ctx.hyper
         mom = h.momentum > 0
@@ -421,6 +432,7 @@ class ZeroOrderFn(torch.autograd.Function):
             return fn(theta.detach().reshape(1, -1)).reshape(())
 
     @staticmethod
+    @once_differentiable
     def backward(ctx, grad_y):
         (theta,) = ctx.saved_tensors
         fn, sigma, num_samples, method, generator = ctx.cfg

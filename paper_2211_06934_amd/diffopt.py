@@ -141,15 +141,19 @@ class SegTable:
     capture: freeing its device memory is not a capturable operation.  The
     tree module caches one table per structure for the life of the process."""
 
-    def __init__(self, handle: int, numel: Sequence[int], offsets, elem_bytes: int):
+    def __init__(self, handle: int, numel: Sequence[int], offsets, elem_bytes: int, total: Optional[int] = None):
         self.handle = handle
         self.numel = list(numel)
         self.offsets = None if offsets is None else list(offsets)
         self.elem_bytes = elem_bytes
+        self._total = total
 
     @property
     def total(self) -> int:
-        return segtable_total(self)
+        """Flat length in elements (read once from the library at creation)."""
+        if self._total is None:
+            self._total = segtable_total(self)
+        return self._total
 
     @property
     def nseg(self) -> int:
@@ -179,7 +183,7 @@ def segtable_create(numel: Sequence[int], offsets: Optional[Sequence[int]] = Non
         o_arr = (ctypes.c_int64 * max(k, 1))(*[int(x) for x in offsets])
     h = ctypes.c_void_p()
     _check(_lib.diffopt_segtable_create(k, n_arr, o_arr, int(elem_bytes), ctypes.byref(h)))
-    return SegTable(h.value, numel, offsets, elem_bytes)
+    return SegTable(h.value, numel, offsets, elem_bytes, int(_lib.diffopt_segtable_total(h.value)))
 
 
 def segtable_destroy(table: SegTable) -> None:
@@ -194,41 +198,65 @@ def segtable_nseg(table: SegTable) -> int:
     return int(_lib.diffopt_segtable_nseg(table.handle))
 
 
+def _tree_sizes(table: SegTable, leaf_ptrs, flat, what: str = "") -> None:
+    """Size checks of one tree's (leaf_ptrs, flat) for the copy kernels.
+
+    A tensor leaf_ptrs must hold one int64 address per leaf of the table, and
+    a tensor flat must have the table's element width and at least
+    table.total elements: the kernels read that many addresses and write or
+    read that many flat elements.  Raw integer addresses are passed through
+    unchecked."""
+    if isinstance(leaf_ptrs, torch.Tensor):
+        if leaf_ptrs.dtype != torch.int64 or leaf_ptrs.numel() != len(table.numel):
+            raise ValueError("%sleaf_ptrs: expected %d int64 leaf addresses, got %d of %s"
+                             % (what, len(table.numel), leaf_ptrs.numel(), leaf_ptrs.dtype))
+    if isinstance(flat, torch.Tensor):
+        if flat.element_size() != table.elem_bytes:
+            raise ValueError("%sflat: the table copies %d-byte elements, flat has %d-byte %s"
+                             % (what, table.elem_bytes, flat.element_size(), flat.dtype))
+        if flat.numel() < table.total:
+            raise ValueError("%sflat: the table needs %d elements, flat has %d" % (what, table.total, flat.numel()))
+
+
+def _tree_operands(table: SegTable, leaf_ptrs, flat, what: str = ""):
+    """Checked addresses of one tree's (leaf_ptrs, flat)."""
+    _tree_sizes(table, leaf_ptrs, flat, what)
+    return _addr(leaf_ptrs, what + "leaf_ptrs", torch.int64), _addr(flat, what + "flat", None)
+
+
 def tree_flatten(table: SegTable, leaf_ptrs, flat, stream=None) -> None:
     """diffopt_tree_flatten: leaf_ptrs is a device int64 tensor of leaf addresses."""
-    _check(_lib.diffopt_tree_flatten(table.handle, _addr(leaf_ptrs, "leaf_ptrs", torch.int64),
-                                     _addr(flat, "flat", None), _stream(stream)))
+    lp, fl = _tree_operands(table, leaf_ptrs, flat)
+    _check(_lib.diffopt_tree_flatten(table.handle, lp, fl, _stream(stream)))
 
 
 def tree_unflatten(table: SegTable, flat, leaf_ptrs, stream=None) -> None:
     """diffopt_tree_unflatten."""
-    _check(_lib.diffopt_tree_unflatten(table.handle, _addr(flat, "flat", None),
-                                       _addr(leaf_ptrs, "leaf_ptrs", torch.int64), _stream(stream)))
+    lp, fl = _tree_operands(table, leaf_ptrs, flat)
+    _check(_lib.diffopt_tree_unflatten(table.handle, fl, lp, _stream(stream)))
 
 
-def _raw_array(items, what, conv):
-    arr = (ctypes.c_void_p * max(len(items), 1))()
-    for i, t in enumerate(items):
-        arr[i] = conv(t, "%s[%d]" % (what, i))
-    return arr
+def _batch_operands(table: SegTable, leaf_ptrs: Sequence, flats: Sequence):
+    if len(leaf_ptrs) != len(flats):
+        raise ValueError("leaf_ptrs and flats need one entry per tree")
+    for t, (lp, fl) in enumerate(zip(leaf_ptrs, flats)):  # every size before any device check
+        _tree_sizes(table, lp, fl, "tree %d: " % t)
+    ops = [_tree_operands(table, lp, fl, "tree %d: " % t) for t, (lp, fl) in enumerate(zip(leaf_ptrs, flats))]
+    lp_arr = (ctypes.c_void_p * max(len(ops), 1))(*[o[0] for o in ops])
+    fl_arr = (ctypes.c_void_p * max(len(ops), 1))(*[o[1] for o in ops])
+    return len(ops), lp_arr, fl_arr
 
 
 def tree_flatten_batch(table: SegTable, leaf_ptrs: Sequence, flats: Sequence, stream=None) -> None:
     """diffopt_tree_flatten_batch: tree t is (leaf_ptrs[t], flats[t])."""
-    if len(leaf_ptrs) != len(flats):
-        raise ValueError("leaf_ptrs and flats need one entry per tree")
-    _check(_lib.diffopt_tree_flatten_batch(
-        table.handle, len(flats), _raw_array(leaf_ptrs, "leaf_ptrs", lambda t, w: _addr(t, w, torch.int64)),
-        _raw_array(flats, "flats", lambda t, w: _addr(t, w, None)), _stream(stream)))
+    k, lp, fl = _batch_operands(table, leaf_ptrs, flats)
+    _check(_lib.diffopt_tree_flatten_batch(table.handle, k, lp, fl, _stream(stream)))
 
 
 def tree_unflatten_batch(table: SegTable, flats: Sequence, leaf_ptrs: Sequence, stream=None) -> None:
     """diffopt_tree_unflatten_batch."""
-    if len(leaf_ptrs) != len(flats):
-        raise ValueError("leaf_ptrs and flats need one entry per tree")
-    _check(_lib.diffopt_tree_unflatten_batch(
-        table.handle, len(flats), _raw_array(flats, "flats", lambda t, w: _addr(t, w, None)),
-        _raw_array(leaf_ptrs, "leaf_ptrs", lambda t, w: _addr(t, w, torch.int64)), _stream(stream)))
+    k, lp, fl = _batch_operands(table, leaf_ptrs, flats)
+    _check(_lib.diffopt_tree_unflatten_batch(table.handle, k, fl, lp, _stream(stream)))
 
 
 def adam_fwd(params, grad, mu, nu, count, lr, b1, b2, eps, eps_root,

@@ -218,3 +218,35 @@ def test_leaf_direct_and_batched_entry_points_in_hip_graph_replay():
         torch.cuda.synchronize()
         for i, (a, b) in enumerate(zip(outs, eager)):
             assert torch.equal(a, b), (rep, i)
+
+
+def test_fused_steps_are_differentiable_once():
+    # the backwards are kernels without an autograd graph: a second-order
+    # meta-gradient through them (create_graph=True, then differentiating the
+    # result) must raise, not silently treat the VJP's inputs as constants.
+    # The loss is quadratic in the step's output, so the cotangent entering
+    # the VJP itself depends on g.
+    import paper_2211_06934_amd as P
+    n = 257
+    rng = np.random.default_rng(11)
+    mk = lambda std: torch.tensor(rng.normal(0, std, n), dtype=torch.float32, device="cuda",  # noqa: E731
+                                  requires_grad=True)
+    p, g = mk(0.05), mk(0.01)
+
+    def second_order_raises(out0):
+        first = torch.autograd.grad((out0 ** 2).sum(), [g], create_graph=True)[0]
+        with pytest.raises(RuntimeError, match="once_differentiable"):
+            torch.autograd.grad(first.sum(), [g])
+
+    opt = P.FlatAdam(lr=LR)
+    p1, _ = opt.step(p, g * 2, opt.init(p.detach()))
+    second_order_raises(p1)
+    table = P.tree.segment_table([(n,)], torch.float32)
+    z = torch.zeros(n, device="cuda")
+    second_order_raises(P.AdamTreeFn.apply(table, 0, P.AdamHyper(), p, g * 2, z, z)[0])
+    second_order_raises(P.SGDTreeFn.apply(table, P.SGDHyper(0.1, 0.9), False, p, g * 2)[0])
+    out = P.RMSPropTreeFn.apply(table, P.RMSPropHyper(), False, p, g * 2, z)
+    second_order_raises(out[0])
+    # first-order meta-gradients are unaffected
+    d = torch.autograd.grad((out[0] ** 2).sum(), [p, g])
+    assert all(torch.isfinite(x).all() for x in d)

@@ -131,8 +131,8 @@ def test_edge_tables():
         t = P.segtable_create(numel)
         assert t.total == 0 and t.nseg == len(numel)
         f = torch.empty(0, dtype=torch.float32, device="cuda")
-        P.tree_flatten(t, torch.zeros(max(len(numel), 1), dtype=torch.int64, device="cuda"), f)
-        P.tree_unflatten(t, f, torch.zeros(max(len(numel), 1), dtype=torch.int64, device="cuda"))
+        P.tree_flatten(t, torch.zeros(len(numel), dtype=torch.int64, device="cuda"), f)
+        P.tree_unflatten(t, f, torch.zeros(len(numel), dtype=torch.int64, device="cuda"))
     # a single leaf is a plain copy, odd length, both layouts
     x = random_bits(1_000_003, np.float32, seed=1)
     _roundtrip([x], 4, "separate", seed=1)

@@ -236,3 +236,32 @@ def test_error_messages_are_per_thread():
         t.join()
     assert all(rc == -1 and "count" in msg for rc, msg in out["count"])
     assert all(rc == -1 and "b1" in msg for rc, msg in out["b1"])
+
+
+def test_tree_copy_bindings_check_operand_sizes_on_host():
+    # the copy kernels read one address per leaf and table.total flat
+    # elements of the table's width: a short address array or a small or
+    # narrower flat buffer is refused before any device call
+    import paper_2211_06934_amd as P
+    d = P.diffopt
+    t = d.SegTable(None, [3, 5], None, 4, total=8)  # host-only stand-in: no device table is needed
+    ok_ptrs = torch.zeros(2, dtype=torch.int64)
+    ok_flat = torch.zeros(8, dtype=torch.float32)
+    cases = [
+        (torch.zeros(1, dtype=torch.int64), ok_flat, "2 int64 leaf addresses"),
+        (torch.zeros(2, dtype=torch.int32), ok_flat, "2 int64 leaf addresses"),
+        (ok_ptrs, torch.zeros(7, dtype=torch.float32), "needs 8 elements"),
+        (ok_ptrs, torch.zeros(8, dtype=torch.float16), "4-byte elements"),
+        (ok_ptrs, torch.zeros(8, dtype=torch.float64), "4-byte elements"),
+    ]
+    for lp, fl, msg in cases:
+        for call in (lambda: P.tree_flatten(t, lp, fl), lambda: P.tree_unflatten(t, fl, lp),
+                     lambda: P.tree_flatten_batch(t, [ok_ptrs, lp], [ok_flat, fl]),
+                     lambda: P.tree_unflatten_batch(t, [ok_flat, fl], [ok_ptrs, lp])):
+            with pytest.raises(ValueError, match=msg):
+                call()
+    # well-sized host tensors get as far as the device check
+    with pytest.raises(ValueError, match="device memory"):
+        P.tree_flatten(t, ok_ptrs, ok_flat)
+    with pytest.raises(ValueError, match="one entry per tree"):
+        P.tree_flatten_batch(t, [ok_ptrs], [ok_flat, ok_flat])
