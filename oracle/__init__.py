@@ -80,6 +80,15 @@ def _configure(lib):
     lib.oracle_es_perturb.restype = None
     lib.oracle_es_estimate.argtypes = [i64, i64, d, d, f64, d]
     lib.oracle_es_estimate.restype = None
+    u64p = ctypes.POINTER(ctypes.c_uint64)
+    lib.oracle_philox4x64_10.argtypes = [u64p, u64p, u64p]
+    lib.oracle_philox4x64_10.restype = None
+    lib.oracle_box_muller.argtypes = [ctypes.c_uint64, d, d]
+    lib.oracle_box_muller.restype = None
+    lib.oracle_es_gaussian_noise.argtypes = [i64, i64, ctypes.c_uint64, d]
+    lib.oracle_es_gaussian_noise.restype = None
+    lib.oracle_es_weights.argtypes = [i64, d, f64, i64, f64, d, d]
+    lib.oracle_es_weights.restype = None
     return lib
 
 
@@ -341,3 +350,56 @@ def es_estimate_mag(noise, weights, scale):
     w = np.abs(_f64(weights))
     Z = np.abs(np.asarray(noise, dtype=np.float64).reshape(w.size, -1))
     return abs(scale) * (w @ Z)
+
+
+def philox4x64_10(counter, key):
+    """One Philox-4x64-10 block: counter (4 uint64 words), key (2 words) -> 4 words."""
+    c = np.ascontiguousarray(np.asarray(counter, dtype=np.uint64).reshape(4))
+    k = np.ascontiguousarray(np.asarray(key, dtype=np.uint64).reshape(2))
+    out = np.empty(4, dtype=np.uint64)
+    u64p = ctypes.POINTER(ctypes.c_uint64)
+    _load().oracle_philox4x64_10(c.ctypes.data_as(u64p), k.ctypes.data_as(u64p), out.ctypes.data_as(u64p))
+    return out
+
+
+def box_muller(word):
+    """The two normals the transform makes of one 64-bit word."""
+    za, zb = ctypes.c_double(), ctypes.c_double()
+    _load().oracle_box_muller(ctypes.c_uint64(int(word)), ctypes.byref(za), ctypes.byref(zb))
+    return za.value, zb.value
+
+
+ES_METHODS = {"plain": 0, "baseline": 1, "antithetic": 2}
+
+
+def es_gaussian_noise(N, n, seed):
+    """The seeded N x n noise matrix of the zero-order estimator, fp64."""
+    z = np.empty((int(N), int(n)))
+    _load().oracle_es_gaussian_noise(int(N), int(n), ctypes.c_uint64(int(seed)), _ptr(z))
+    return z
+
+
+def es_weights(fvals, method, sigma, f0=0.0):
+    """(w, scale) of the estimate from the evaluations: plain, baseline (f0 =
+    f(theta)) or antithetic (fvals holds the N plus-points, then the N minus-points)."""
+    m = ES_METHODS[method]
+    f = _f64(fvals)
+    N = f.size // 2 if m == 2 else f.size
+    if m == 2 and f.size != 2 * N:
+        raise ValueError("antithetic needs 2N evaluations")
+    w = np.empty(N)
+    scale = ctypes.c_double()
+    _load().oracle_es_weights(N, _ptr(f), float(f0), m, float(sigma), _ptr(w), ctypes.byref(scale))
+    return w, scale.value
+
+
+def es_weight_terms(fvals, method, f0=0.0):
+    """|terms| of each weight (tolerance scales): |f_i|, |f_i| + |f0| or |f_i| + |f_{N+i}|."""
+    f = np.abs(_f64(fvals))
+    m = ES_METHODS[method]
+    if m == 0:
+        return f
+    if m == 1:
+        return f + abs(float(f0))
+    N = f.size // 2
+    return f[:N] + f[N:]

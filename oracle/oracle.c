@@ -51,6 +51,14 @@
  *             exactly 0 since the update vanishes for every v >= 0.
  *   unrolled: fp64 central differences of the K-step map.
  *   pack    : numpy concatenation, bit for bit; unpack(pack(x)) == x.
+ *   noise   : Philox-4x64-10 bit for bit against numpy's independent
+ *             implementation (numpy.random.Philox); the Box-Muller transform
+ *             against its closed-form values (u1 = 1, u1 = 2^-k at the angles
+ *             0, pi/4, pi/2, pi, 3 pi/2); the composed noise against the
+ *             standard normal (moments, Kolmogorov-Smirnov, tails) and the
+ *             independence of each element from N and n.
+ *   ES      : exact recovery of linear and quadratic gradients with a
+ *             symmetric orthonormal sample set, for every weighting method.
  *   mag_*   : the tolerance scales are sums of absolute values of terms.
  *             From below they bound |value| (triangle inequality); from
  *             above they equal |value| on inputs whose terms all share one
@@ -457,4 +465,109 @@ void oracle_es_estimate(int64_t N, int64_t n, const double* noise, const double*
     for (int64_t i = 0; i < N; ++i) acc += w[i] * noise[i * n + j];
     grad[j] = scale * acc;
   }
+}
+
+/* ---------------------------------------------------------------------------
+ * Gaussian noise for the zero-order estimator, drawn from a counter-based
+ * generator so that every element z_ij (sample i, parameter j) is a pure
+ * function of (seed, i, j): the noise never has to be stored, and either
+ * side regenerates any element on its own.  Sec. 2.2 / Listing 3 make the
+ * noise sampler part of the estimator; the paper names no generator, so this
+ * is a reading (its published sources are named below).
+ *
+ * Philox-4x64-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers:
+ * as easy as 1, 2, 3", SC 2011): a 256-bit counter block c = (c0..c3) and a
+ * 128-bit key k = (k0, k1) go through ten rounds; each round forms the full
+ * 128-bit products M0 c0 = (hi0, lo0) and M1 c2 = (hi1, lo1) and maps
+ *   c <- (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0),
+ * and between rounds the key advances by the Weyl increments W0, W1
+ * (wrapping).  The four words of the last round are the output block.
+ */
+#define PHILOX_M0 0xD2E7470EE14C6C93ull
+#define PHILOX_M1 0xCA5A826395121157ull
+#define PHILOX_W0 0x9E3779B97F4A7C15ull
+#define PHILOX_W1 0xBB67AE8584CAA73Bull
+
+void oracle_philox4x64_10(const uint64_t* ctr, const uint64_t* key, uint64_t* out) {
+  uint64_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+  uint64_t k0 = key[0], k1 = key[1];
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += PHILOX_W0;
+      k1 += PHILOX_W1;
+    }
+    unsigned __int128 p0 = (unsigned __int128)PHILOX_M0 * c0;
+    unsigned __int128 p1 = (unsigned __int128)PHILOX_M1 * c2;
+    uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0;
+    uint64_t hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+    uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  out[0] = c0;
+  out[1] = c1;
+  out[2] = c2;
+  out[3] = c3;
+}
+
+/*
+ * Box-Muller transform (Box and Muller, 1958) of one 64-bit word: its low
+ * 32 bits give u1 = (floor(lo / 2^8) + 1) 2^-24 in (0, 1], its high 32 bits
+ * u2 = floor(hi / 2^8) 2^-24 in [0, 1) (24-bit uniforms, exact in fp32 and
+ * fp64), and
+ *   r = sqrt(-2 ln u1),   za = r cos(2 pi u2),   zb = r sin(2 pi u2)
+ * are two independent standard normal draws.
+ */
+void oracle_box_muller(uint64_t word, double* za, double* zb) {
+  uint32_t lo = (uint32_t)word, hi = (uint32_t)(word >> 32);
+  double u1 = ((double)(lo >> 8) + 1.0) * 0x1p-24;
+  double u2 = (double)(hi >> 8) * 0x1p-24;
+  double r = sqrt(-2.0 * log(u1));
+  double a = 6.283185307179586476925 * u2; /* 2 pi, rounded to double */
+  *za = r * cos(a);
+  *zb = r * sin(a);
+}
+
+/*
+ * The noise matrix z (N x n, row-major) for a seed: element j of sample i
+ * takes word (j mod 8) / 2 of the Philox block at counter (j / 8, i, 0, 0)
+ * under key (seed, 0), through the Box-Muller transform above: za for even
+ * j, zb for odd j.  Eight consecutive elements share one block.
+ */
+void oracle_es_gaussian_noise(int64_t N, int64_t n, uint64_t seed, double* z) {
+  uint64_t key[2] = {seed, 0};
+  for (int64_t i = 0; i < N; ++i)
+    for (int64_t b = 0; b * 8 < n; ++b) {
+      uint64_t ctr[4] = {(uint64_t)b, (uint64_t)i, 0, 0}, out[4];
+      oracle_philox4x64_10(ctr, key, out);
+      for (int64_t e = 0; e < 8 && b * 8 + e < n; ++e) {
+        double za, zb;
+        oracle_box_muller(out[e / 2], &za, &zb);
+        z[i * n + b * 8 + e] = (e % 2 == 0) ? za : zb;
+      }
+    }
+}
+
+/*
+ * Weights and scale of the Monte-Carlo estimate from the caller's
+ * evaluations f (reading 17 of the design notes):
+ *   method 0, plain:      w_i = f_i,              scale = 1 / (N s)    (f has N values)
+ *   method 1, baseline:   w_i = f_i - f0,         scale = 1 / (N s)    (f0 = f(theta))
+ *   method 2, antithetic: w_i = f_i - f_{N+i},    scale = 1 / (2 N s)  (f has 2N values:
+ *                         the points theta + s z_i, then theta - s z_i)
+ * so that grad = scale * sum_i w_i z_i (oracle_es_estimate).
+ */
+void oracle_es_weights(int64_t N, const double* f, double f0, int64_t method, double sigma, double* w,
+                       double* scale) {
+  for (int64_t i = 0; i < N; ++i) {
+    if (method == 0)
+      w[i] = f[i];
+    else if (method == 1)
+      w[i] = f[i] - f0;
+    else
+      w[i] = f[i] - f[N + i];
+  }
+  *scale = 1.0 / ((method == 2 ? 2.0 : 1.0) * (double)N * sigma);
 }

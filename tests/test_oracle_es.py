@@ -69,3 +69,110 @@ def test_antithetic_estimate_converges_to_smoothed_gradient():
     g = oracle.es_estimate(Z, fv[:N] - fv[N:], 1.0 / (2 * N * sigma))
     err = np.linalg.norm(g - grad(theta)) / np.linalg.norm(grad(theta))
     assert err < 5 * np.sqrt(n / N) * 3
+
+
+# ------------------------------------------------------------------ seeded noise
+# The noise is drawn from Philox-4x64-10 through the Box-Muller transform.  The
+# generator is pinned bit for bit to numpy's independent implementation, the
+# transform to its closed-form values, and the composed noise to the normal
+# distribution and to the structure a counter-based design guarantees.
+
+def _numpy_philox_block(counter, key):
+    """numpy's Philox advances its 256-bit counter before each block, so the
+    block at counter c is its first output when started at c - 1."""
+    c = [int(x) for x in counter]
+    v = (c[0] | c[1] << 64 | c[2] << 128 | c[3] << 192) - 1
+    start = np.array([(v >> (64 * i)) & ((1 << 64) - 1) for i in range(4)], dtype=np.uint64)
+    gen = np.random.Philox(counter=start, key=np.array(key, dtype=np.uint64))
+    return gen.random_raw(4).astype(np.uint64)
+
+
+def test_philox_matches_numpy_bit_for_bit():
+    rng = np.random.default_rng(2211)
+    cases = [([1, 0, 0, 0], [0, 0]), ([0, 1, 0, 0], [0, 0]), ([0, 0, 0, 1], [2**64 - 1, 2**64 - 1]),
+             ([2**64 - 1, 2**64 - 1, 2**64 - 1, 2**64 - 1], [12345, 67890])]
+    for _ in range(200):
+        cases.append(([int(x) for x in rng.integers(0, 2**64, size=4, dtype=np.uint64)],
+                      [int(x) for x in rng.integers(0, 2**64, size=2, dtype=np.uint64)]))
+    for ctr, key in cases:
+        assert np.array_equal(oracle.philox4x64_10(ctr, key), _numpy_philox_block(ctr, key)), (ctr, key)
+    # consecutive blocks of one numpy stream are consecutive counters (with the
+    # carry from word 0 into word 1)
+    gen = np.random.Philox(counter=np.array([2**64 - 3, 5, 0, 0], dtype=np.uint64),
+                           key=np.array([7, 9], dtype=np.uint64))
+    raw = gen.random_raw(16).astype(np.uint64).reshape(4, 4)
+    for b, ctr in enumerate(([2**64 - 2, 5, 0, 0], [2**64 - 1, 5, 0, 0], [0, 6, 0, 0], [1, 6, 0, 0])):
+        assert np.array_equal(oracle.philox4x64_10(ctr, [7, 9]), raw[b]), b
+
+
+def _word(lo, hi):
+    return (int(hi) << 32) | int(lo)
+
+
+def test_box_muller_closed_forms():
+    # u1 = 1 gives r = 0: both normals are exactly zero
+    assert oracle.box_muller(_word(0xFFFFFFFF, 0x12345678)) == (0.0, 0.0)
+    for k in (1, 2, 7, 24):
+        lo = ((1 << (24 - k)) - 1) << 8  # u1 = 2^-k exactly
+        r = np.sqrt(2.0 * k * np.log(2.0))
+        for hi, za, zb in ((0, r, 0.0),                      # u2 = 0
+                           (1 << 29, r / np.sqrt(2), r / np.sqrt(2)),  # u2 = 1/8
+                           (1 << 30, 0.0, r),                # u2 = 1/4
+                           (1 << 31, -r, 0.0),               # u2 = 1/2
+                           (3 << 30, 0.0, -r)):              # u2 = 3/4
+            ga, gb = oracle.box_muller(_word(lo, hi))
+            assert abs(ga - za) <= 1e-14 * r and abs(gb - zb) <= 1e-14 * r, (k, hi, ga, gb, za, zb)
+            # the low 8 bits of each half do not enter the 24-bit uniforms
+            assert oracle.box_muller(_word(lo | 0xFF, hi | 0xFF)) == (ga, gb)
+
+
+def test_gaussian_noise_is_standard_normal():
+    from scipy import stats
+    N, n = 64, (1 << 14) + 5
+    z = oracle.es_gaussian_noise(N, n, 20221112).reshape(-1)
+    M = z.size
+    assert abs(z.mean()) < 5 / np.sqrt(M)
+    assert abs(z.var() - 1.0) < 5 * np.sqrt(2.0 / M)
+    assert stats.kstest(z, "norm").pvalue > 1e-4
+    # the two normals of one word, and neighbouring words, are uncorrelated
+    pairs = z[: M // 2 * 2].reshape(-1, 2)
+    assert abs(np.corrcoef(pairs[:, 0], pairs[:, 1])[0, 1]) < 5 / np.sqrt(M / 2)
+    assert abs(np.corrcoef(z[:-2], z[2:])[0, 1]) < 5 / np.sqrt(M)
+    # the tails: P(|z| > 3) = 0.0026998
+    assert abs(np.mean(np.abs(z) > 3.0) - 0.0026998) < 5 * np.sqrt(0.0027 / M)
+
+
+def test_gaussian_noise_is_a_function_of_seed_sample_and_element():
+    a = oracle.es_gaussian_noise(9, 101, 5)
+    assert np.array_equal(oracle.es_gaussian_noise(9, 37, 5), a[:, :37])   # element j does not depend on n
+    assert np.array_equal(oracle.es_gaussian_noise(4, 101, 5), a[:4])     # sample i does not depend on N
+    b = oracle.es_gaussian_noise(9, 101, 6)
+    assert not np.any(a == b)
+    assert not np.any(a[0] == a[1])
+
+
+def test_weights_recover_linear_and_quadratic_gradients_exactly():
+    # with the symmetric sample set {+sqrt(n) e_j} u {-sqrt(n) e_j}, sum_i z_i = 0
+    # and (1/N) sum_i z_i z_i^T = I, so each method's weights and scale must
+    # return the gradient of a linear function exactly, and antithetic that of
+    # a quadratic
+    n = 12
+    a = normal(n, 1.0, "es", "grad", 7).astype(np.float64)
+    theta = normal(n, 1.0, "es", "p0", 7).astype(np.float64)
+    Z = np.sqrt(n) * np.concatenate([np.eye(n), -np.eye(n)])
+    N = Z.shape[0]
+    lin = lambda x: x @ a + 0.75  # noqa: E731
+    f_quad, grad_quad = _quadratic(n, 9)
+    for sigma in (1e-2, 0.5):
+        plus = oracle.es_perturb(theta, Z, sigma, antithetic=True)
+        for method, f, want in (("plain", lin, a), ("baseline", lin, a), ("antithetic", lin, a),
+                                ("antithetic", f_quad, grad_quad(theta))):
+            fv = np.array([f(x) for x in (plus if method == "antithetic" else plus[:N])])
+            w, scale = oracle.es_weights(fv, method, sigma, f0=f(theta))
+            g = oracle.es_estimate(Z, w, scale)
+            assert np.max(np.abs(g - want)) < 1e-9 * np.max(np.abs(want)), (method, sigma)
+    # baseline and plain differ by the f0 term only
+    fv = np.array([lin(x) for x in oracle.es_perturb(theta, Z, 0.1)])
+    assert np.allclose(oracle.es_weights(fv, "baseline", 0.1, f0=2.0)[0], fv - 2.0, rtol=0, atol=0)
+    assert oracle.es_weights(fv, "plain", 0.1)[1] == 1.0 / (N * 0.1)
+    assert oracle.es_weights(np.concatenate([fv, fv]), "antithetic", 0.1)[1] == 1.0 / (2 * N * 0.1)

@@ -160,6 +160,17 @@ def es_pins():
     for scale in (0.3, -2.0):
         out.append(("es estimate scale %g" % scale,
                     _same(oracle.es_estimate(Z, w, scale), oracle.es_estimate_mag(Z, w, scale))))
+    # weights formed from evaluations: f_i of the sign of z_i, and the
+    # subtracted f0 or f_{N+i} of the other sign
+    Zp = np.abs(Z)
+    f = np.abs(rng.normal(0, 1, 2 * Nn)) + 0.1
+    f[Nn:] *= -1.0
+    for method, fv, f0 in (("plain", f[:Nn], 0.0), ("baseline", f[:Nn], -0.7), ("antithetic", f, 0.0)):
+        wm, sc = oracle.es_weights(fv, method, 0.05, f0=f0)
+        terms = oracle.es_weight_terms(fv, method, f0=f0)
+        out.append(("es weights %s" % method, _same(wm, terms)))
+        out.append(("es estimate %s" % method,
+                    _same(oracle.es_estimate(Zp, wm, sc), oracle.es_estimate_mag(Zp, terms, sc))))
     return out
 
 
@@ -263,6 +274,9 @@ PY_MUTANTS = {
         + _double_terms("mag_dg = mag_T + (abs(lr) * dP if nesterov else 0.0)", ["abs(lr) * dP"])
         + _double_terms("return mag_dg, momentum * mag_T", ["momentum * mag_T"])),
     "es_estimate_mag": [("return abs(scale) * (w @ Z)", "return abs(scale) * (w @ Z + w[0] * Z[0])")],
+    "es_weight_terms": [("return f + abs(float(f0))", "return f + 2.0 * abs(float(f0))"),
+                        ("return f[:N] + f[N:]", "return 2.0 * f[:N] + f[N:]"),
+                        ("return f[:N] + f[N:]", "return f[:N] + 2.0 * f[N:]")],
 }
 
 
