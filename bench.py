@@ -1,22 +1,35 @@
 """Benchmark of the differentiable-Adam hot path on one MI355X.
 
-One step = one pass of the whole path over one batch of synthetic input:
-  tree flatten of the params tree and of K gradient trees (one batched launch)
-  -> K-step unrolled Adam forward (the K steps fused in one kernel per 16
-     steps, running params in registers; by default only the final moment
-     state is stored, --trajectory stored keeps every one)
-  -> K-step unrolled Adam backward (the same, running cotangents in registers,
-     the moments recomputed from the nearest stored state)
-  -> tree unflatten of p_K and of the K gradient cotangents (one batched launch).
-Default workload: the many-small-tensor tree (20,000 fp32 leaves, log-uniform
-sizes in [1, 65536], K = 3).  All inputs are resident in HBM before timing.
-Other workloads:
-  tiny_mlp | convnet32 | resnet18_k1 | resnet18_k10   the same step on other trees
-  flat_1b [_zero_mv]       one interior fwd + bwd on a 10^9-element buffer
-                           (_zero_mv: zero moment cotangents)
-  many_small_treemap       the K-step pass leaf-direct, without flatten/unflatten
-  many_small_stepwise      the same pass with one launch per Adam step (the form
-                           a live inner loop needs)
+Default (the metric's own measure, on its largest single-GPU configuration):
+one interior Adam step on a flat buffer of 10^9 fp32 parameters at count 100
+-- the fused forward (p, g, m, v -> p', m', v': 28 B/element) and its fused
+VJP with all three cotangents (dP, dM, dV, g, m, v -> dg, dm, dv: 36 B/element)
+-- timed with HIP events; `value` is parameters per second of the fwd + bwd
+pair and `roofline` covers the VJP, the longer of the two kernels.  Outside
+the timed region every one of the 10^9 elements of all six outputs is copied
+back in 2^24-element chunks and checked against the CPU oracle (1e-5 of the
+term scale forward, 1e-4 backward); the oracle's own time over those chunks
+is `cpu_baseline`.  A mismatch fails the run.
+
+The same line carries `legs`: the 20,000-leaf tree (n = 117,000,292, K = 3)
+in four forms, each with its own time and bytes per element:
+  stepwise           pack p + K grads -> K single-step fwd launches -> K
+                     single-step VJP launches -> unpack p_K + K dg (the
+                     live-loop form, every gradient may depend on the previous
+                     step: 248 B/element)
+  treemap_stepwise   the same steps leaf-direct, no pack/unpack (the kernels
+                     MetaAdam launches: 184 B/element)
+  fused              pack -> K steps fused in one forward and one VJP launch,
+                     trajectory recomputed -> unpack (valid only when all K
+                     gradients are known before the first step: 144 B/element)
+  treemap_fused      the fused form leaf-direct (80 B/element)
+
+Other workloads (--workload), each printing its own line:
+  many_small | tiny_mlp | convnet32 | resnet18_k1 | resnet18_k10
+                           pack -> fused K-step fwd -> fused K-step bwd -> unpack
+  flat_1b_zero_mv          the 10^9 step with zero moment cotangents
+  many_small_treemap       the fused K-step pass leaf-direct
+  many_small_stepwise      the stepwise pass alone
   sgd_flat | rmsprop_flat | sgd_treemap | rmsprop_treemap
                            one fwd + bwd of the other fused optimizers
   es_resnet18              ES perturb + estimate at the ResNet-18 size
@@ -25,12 +38,7 @@ Other workloads:
 --graph replays one captured step as a HIP graph (the small trees are
 launch-bound).
 
-Prints ONE JSON line.  `value` is Adam fwd+bwd parameter-steps per second for
-the whole pass (n * K / step time); `roofline` covers the dominant kernel
-(by time), timed with HIP events on the launch stream around its launches.
-`cpu_baseline` times the CPU oracle on a bounded sample of the same work.
-
-    python bench.py [--steps 20] [--warmup 3] [--workload many_small]
+    python bench.py [--steps 20] [--warmup 3] [--workload flat_1b]
 """
 from __future__ import annotations
 
@@ -117,7 +125,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="many_small",
+    ap.add_argument("--workload", default="flat_1b",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
                              "many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
                              "es_resnet18", "adam_vs_torch", "flat_1b_zero_mv", "many_small_stepwise"])
@@ -126,7 +134,9 @@ def parse():
                          "(and every %d-th) and let the backward recompute the rest in registers" % REMAT_SPAN)
     ap.add_argument("--graph", action="store_true",
                     help="capture one step in a HIP graph and time replays (no per-phase split)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle leg (flat_1b: also the full-size oracle check)")
+    ap.add_argument("--no-legs", action="store_true", help="flat_1b: skip the 20,000-leaf legs")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     return ap.parse_args()
 
@@ -300,9 +310,10 @@ def phases_tree(S):
     ]
 
 
-def setup_treemap(torch, P, w, trajectory):
+def setup_treemap(torch, P, w, trajectory, stepwise=False):
     """Leaf-direct form of the same pass: every operand is a tree of separately
-    allocated leaves; no flatten or unflatten."""
+    allocated leaves; no flatten or unflatten.  stepwise: also the K - 1
+    intermediate parameter trees, for one launch per step."""
     from workloads import HYPER, torch_normal
     K, n, numel = w.K, w.n, w.numels
     dev = "cuda"
@@ -330,9 +341,49 @@ def setup_treemap(torch, P, w, trajectory):
     S["pK"] = tree()
     S["dg"] = [tree() for _ in range(K)]
     S["dm0"], S["dv0"] = tree(), tree()
+    if stepwise:
+        S["p_steps"] = [S["p0"]] + [tree() for _ in range(K - 1)] + [S["pK"]]
     S["keep"] = trees
     torch.cuda.synchronize()
     return S
+
+
+def step_treemap_stepwise(P, S, ev=None):
+    """The leaf-direct pass one launch per step (the kernels MetaAdam runs):
+    K single-step forward launches, then K single-step VJP launches, the
+    first with zero moment cotangents."""
+    h = S["hyper"]
+    K, T = S["K"], S["table"]
+    co = (h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+    ps, mu, nu = S["p_steps"], S["mu"], S["nu"]
+    if ev:
+        ev[0].record()
+    for k in range(K):
+        P.adam_fwd_tree(T, ps[k], S["g"][k], mu[k], nu[k], S["count0"] + k, *co, ps[k + 1], mu[k + 1], nu[k + 1])
+    if ev:
+        ev[1].record()
+    for k in range(K - 1, -1, -1):
+        first = k == K - 1
+        P.adam_bwd_tree(T, S["cot"], None if first else S["dm0"], None if first else S["dv0"], S["g"][k], mu[k],
+                        nu[k], S["count0"] + k, *co, S["dg"][k], S["dm0"], S["dv0"])
+    if ev:
+        ev[2].record()
+
+
+def phases_treemap_stepwise(S):
+    K, n = S["K"], S["n"]
+    return [("adam_fwd_tree", "adam_fwd_tree", K, K * B_FWD * n),
+            ("adam_bwd_tree", "adam_bwd_tree", K, (K * B_BWD - (B_BWD - B_BWD_ZERO_MV)) * n)]
+
+
+def trajectory_label(S):
+    """Which moment states the forward stores, from the setup itself."""
+    K, stored = S["K"], set(S["stored"])
+    if stored >= set(range(1, K + 1)):
+        return "every moment state stored"
+    kept = sorted(stored - {K})
+    return ("final moment state stored%s; the VJP recomputes the others from the nearest stored state"
+            % ("" if not kept else " and states %s" % ", ".join(map(str, kept))))
 
 
 def step_treemap(P, S, ev=None):
@@ -647,30 +698,285 @@ def host_cpu_model():
     return platform.processor() or platform.machine()
 
 
-def cpu_baseline_flat_1b(w, target_s):
+RTOL_FWD = 1e-5  # per-element bars against the oracle's term scale (mag)
+RTOL_BWD = 1e-4
+ORACLE_CHUNK = 1 << 24  # elements per chunk of the timed oracle pass
+CHECK_CHUNK = 1 << 22   # elements per task of the comparison pass
+
+
+def _flat_operands(S):
+    ins = ["p", "g", "m", "v", "dP"] + ([] if S.get("zero_mv") else ["dM", "dV"])
+    return ins, ["po", "mo", "vo", "dg", "dm", "dv"]
+
+
+def _oracle_hyper(S):
+    h = S["hyper"]
+    return (S["count0"], h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
+
+
+def oracle_time_flat(torch, S, chunk=ORACLE_CHUNK, progress=None):
+    """The CPU oracle over the whole flat step, timed: the inputs are copied
+    back in chunks of `chunk` elements and upcast to fp64, then the oracle runs
+    the forward and the VJP on each chunk in one thread; only those two calls
+    are timed."""
     import numpy as np
     import oracle
-    from workloads import HYPER, abs_normal, normal
-    h = dict(HYPER, eps_root=w.eps_root)
-
-    def run(n):
-        p, g = normal(n, 0.05, "cpu", "p0").astype(np.float64), normal(n, w.grad_std, "cpu", "grad").astype(np.float64)
-        m, v = abs_normal(n, 1e-4, "cpu", "mu").astype(np.float64), abs_normal(n, 1e-4, "cpu", "nu").astype(np.float64)
-        dP, dM, dV = (normal(n, 1.0, "cpu", t).astype(np.float64) for t in ("cot_p", "cot_m", "cot_v"))
+    n, hy = S["n"], _oracle_hyper(S)
+    ins, _ = _flat_operands(S)
+    host = {k: torch.empty(min(chunk, n), dtype=torch.float32, pin_memory=torch.cuda.is_available()) for k in ins}
+    t_oracle, nchunks = 0.0, 0
+    for c0 in range(0, n, chunk):
+        c1 = min(n, c0 + chunk)
+        for k in ins:
+            host[k][:c1 - c0].copy_(S[k][c0:c1])
+        x = {k: host[k][:c1 - c0].numpy().astype(np.float64) for k in ins}
         t0 = time.perf_counter()
-        oracle.adam_fwd(p, g, m, v, w.count0, h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
-        oracle.adam_bwd(dP, dM, dV, g, m, v, w.count0, h["lr"], h["b1"], h["b2"], h["eps"], h["eps_root"])
-        return time.perf_counter() - t0
+        oracle.adam_fwd(x["p"], x["g"], x["m"], x["v"], *hy)
+        oracle.adam_bwd(x["dP"], x.get("dM"), x.get("dV"), x["g"], x["m"], x["v"], *hy)
+        t_oracle += time.perf_counter() - t0
+        nchunks += 1
+        if progress and (nchunks % 15 == 0 or c1 == n):
+            progress("oracle timing: %d of %d elements, %.1f s" % (c1, n, t_oracle))
+    return {"value": float("%.4g" % (n / t_oracle)), "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": "all %d elements, one fwd + one bwd at count %d, in %d chunks of %d copied back from the "
+                      "device; fp64, single thread; %.1f s of oracle time (copies and conversions excluded)"
+                      % (n, S["count0"], nchunks, chunk, t_oracle),
+            "seconds": round(t_oracle, 2), "host_cpu": host_cpu_model(), "host_threads": os.cpu_count()}
 
-    t_small = run(1 << 20)
-    n = int(min(w.n, (1 << 20) / max(t_small, 1e-9) * target_s))
-    t = run(n)
-    return {"value": n / t, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": "first %d of %d params, one fwd+bwd step; fp64 single thread; %.1f s" % (n, w.n, t),
-            "seconds": t, "host_cpu": host_cpu_model(), "host_threads": os.cpu_count()}
+
+def oracle_check_flat(torch, S, chunk=CHECK_CHUNK, workers=None, progress=None):
+    """Every element of the flat step's six outputs against the CPU oracle.
+
+    The element range is cut into tasks of `chunk` elements, run by a pool of
+    host threads (the oracle's C calls and numpy's array loops release the
+    interpreter lock).  Per task the inputs and outputs are copied back, the
+    oracle computes the forward and the VJP in fp64 from the same fp32 inputs
+    together with its term scales, and each output element must lie within
+    rtol * mag of the oracle's value.  NaN or inf from the GPU fails."""
+    import concurrent.futures
+    import threading
+    import numpy as np
+    import oracle
+    n, hy = S["n"], _oracle_hyper(S)
+    ins, outs = _flat_operands(S)
+    rtol = {"po": RTOL_FWD, "mo": RTOL_FWD, "vo": RTOL_FWD, "dg": RTOL_BWD, "dm": RTOL_BWD, "dv": RTOL_BWD}
+    if workers is None:
+        workers = max(1, min(12, (os.cpu_count() or 2) - 1))
+    local = threading.local()
+    lock = threading.Lock()
+    done = [0]
+
+    def task(c0):
+        c1 = min(n, c0 + chunk)
+        L = c1 - c0
+        if not hasattr(local, "host"):
+            local.host = {k: torch.empty(chunk, dtype=torch.float32, pin_memory=torch.cuda.is_available())
+                          for k in ins + outs}
+        h = local.host
+        for k in ins + outs:
+            h[k][:L].copy_(S[k][c0:c1])
+        x = {k: h[k][:L].numpy().astype(np.float64) for k in ins}
+        dM, dV = x.get("dM"), x.get("dV")
+        po, mo, vo, _ = oracle.adam_fwd(x["p"], x["g"], x["m"], x["v"], *hy)
+        _, dg, dm, dv = oracle.adam_bwd(x["dP"], dM, dV, x["g"], x["m"], x["v"], *hy)
+        mp, mm, mv, _ = oracle.adam_fwd_mag(x["p"], x["g"], x["m"], x["v"], *hy)
+        mg, mdm, mdv = oracle.adam_bwd_mag(x["dP"], dM, dV, x["g"], x["m"], x["v"], *hy)
+        res = {}
+        for k, ref, mag in (("po", po, mp), ("mo", mo, mm), ("vo", vo, mv), ("dg", dg, mg), ("dm", dm, mdm),
+                            ("dv", dv, mdv)):
+            got = h[k][:L].numpy()
+            err = np.subtract(got, ref)
+            np.abs(err, out=err)
+            np.divide(err, np.maximum(mag, 1e-300), out=err)  # error in units of the term scale
+            ok = err <= rtol[k]  # NaN compares false
+            nb = L - int(np.count_nonzero(ok))
+            first = None
+            if nb:
+                i = int(np.flatnonzero(~ok)[0])
+                first = {"output": k, "index": c0 + i, "got": float(got[i]), "oracle": float(ref[i]),
+                         "mag": float(mag[i])}
+            res[k] = (nb, float(np.nanmax(err)) if nb < L else float("nan"), first)
+        with lock:
+            done[0] += L
+            if progress and (done[0] // chunk) % 40 == 0:
+                progress("oracle check: %d of %d elements" % (done[0], n))
+        return c0, res
+
+    t0 = time.perf_counter()
+    bad = {k: 0 for k in outs}
+    worst = {k: 0.0 for k in outs}
+    first_bad = None
+    with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+        for c0, res in sorted(ex.map(task, range(0, n, chunk)), key=lambda r: r[0]):
+            for k, (nb, wq, first) in res.items():
+                bad[k] += nb
+                worst[k] = max(worst[k], wq) if wq == wq else float("nan")
+                if first is not None and first_bad is None:
+                    first_bad = first
+    if progress:
+        progress("oracle check: %d elements, %d failures, %.1f s" % (n, sum(bad.values()), time.perf_counter() - t0))
+    return {"elements": n, "outputs": outs, "rtol_fwd": RTOL_FWD, "rtol_bwd": RTOL_BWD, "bar": "|gpu - oracle| <= "
+            "rtol * mag per element, mag = the oracle's sum of |terms| of the result", "failures": sum(bad.values()),
+            "failures_per_output": bad, "max_err_over_mag": {k: float("%.3g" % v) for k, v in worst.items()},
+            "first_failure": first_bad, "threads": workers, "chunk": chunk,
+            "wall_s": round(time.perf_counter() - t0, 1)}
+
+
+def placement(S, names):
+    """Base address of each operand modulo 2 MiB and 1 GiB (virtual addresses)."""
+    out = {}
+    for k in names:
+        if S.get(k) is not None:
+            a = S[k].data_ptr()
+            out[k] = {"mod_2MiB": a % (1 << 21), "mod_1GiB": a % (1 << 30), "GiB": a >> 30}
+    return out
 
 
 # ---------------------------------------------------------------------- main
+
+
+def log(msg):
+    """Progress on stderr (the JSON line is the only stdout output)."""
+    sys.stderr.write("bench: %s\n" % msg)
+    sys.stderr.flush()
+
+
+def time_workload(torch, P, S, step, phases, steps, warmup, graph=False):
+    """Warm up, then time `steps` steps: HIP events around every phase of every
+    step (eager), or around `steps` replays of one captured step (graph).
+    Returns (phase table, ms per step, per-phase ms or None)."""
+    ph = phases(S)
+    nph = len(ph)
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        step(P, S)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    phase_ms = None
+    if graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step(P, S)
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step(P, S)
+        g.replay()
+        torch.cuda.synchronize()
+        t_start.record()
+        for _ in range(steps):
+            g.replay()
+        t_end.record()
+        torch.cuda.synchronize()
+    else:
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t_start.record()
+        for k in range(steps):
+            step(P, S, evs[k])
+        t_end.record()
+        torch.cuda.synchronize()
+        phase_ms = [sum(e[i].elapsed_time(e[i + 1]) for e in evs) / steps for i in range(nph)]
+    return ph, t_start.elapsed_time(t_end) / steps, phase_ms
+
+
+def summarize(ph, ms_step, phase_ms, n, K, traffic_key):
+    """Per-phase rates and the dominant phase's roofline entry: algorithmic
+    bytes per launch over that phase's average launch time."""
+    breakdown, roofline = {}, None
+    if phase_ms is None:
+        return breakdown, roofline
+    for (name, kern, launches, byts), t in zip(ph, phase_ms):
+        breakdown[name] = {"ms": round(t, 4), "launches": launches,
+                           "GB/s": round(byts / (t * 1e-3) / 1e9, 1),
+                           "frac": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        if "fwd" in name or "bwd" in name:  # parameter-steps per second of this phase alone
+            breakdown[name]["G_params_per_s"] = round(n * K / (t * 1e-3) / 1e9, 2)
+    dom = max(range(len(ph)), key=lambda i: phase_ms[i])
+    dname, dkern, dlaunch, dbytes = ph[dom]
+    avg_launch_s = phase_ms[dom] * 1e-3 / dlaunch
+    per_launch = dbytes / dlaunch
+    achieved = per_launch / avg_launch_s / 1e9
+    traffic = traffic_from_profile(dkern, traffic_key, per_launch)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "traffic_source": (None if traffic is None else
+                                   "profiles/traffic_%s_%s.json: rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, of the "
+                                   "same command, scaled by the counts for a 1 GiB copy; reported only while the "
+                                   "kernel sources and the per-launch bytes match" % (dkern, traffic_key)),
+                "kernel": dkern, "bytes_per_launch": int(per_launch),
+                "avg_launch_us": round(avg_launch_s * 1e6, 2)}
+    return breakdown, roofline
+
+
+# the 20,000-leaf tree in four forms, timed beside the flat 10^9 step
+LEGS = (
+    ("stepwise", "live-loop: one launch per Adam step, so each gradient may depend on the previous step",
+     "many_small_stepwise",
+     "flatten p + K grads -> K single-step Adam fwd launches -> K single-step Adam VJP launches -> "
+     "unflatten p_K + K dg"),
+    ("treemap_stepwise", "live-loop: one leaf-direct launch per Adam step, the kernels MetaAdam runs "
+     "(leaf-address arrays built once)", "many_small_treemap_stepwise",
+     "K single-step leaf-direct Adam fwd launches -> K single-step leaf-direct Adam VJP launches, no pack/unpack"),
+    ("fused", "fixed-gradient: all K gradients known before the first step, K steps fused per launch",
+     "many_small",
+     "flatten p + K grads -> fused K-step Adam fwd -> fused K-step Adam VJP -> unflatten p_K + K dg"),
+    ("treemap_fused", "fixed-gradient, leaf-direct: K steps fused per launch, no pack/unpack",
+     "many_small_treemap", "leaf-direct fused K-step Adam fwd -> fused K-step Adam VJP"),
+)
+
+
+def leg_setup(name, torch, P, w):
+    if name == "stepwise":
+        return setup_stepwise(torch, P, w), step_stepwise, phases_stepwise
+    if name == "treemap_stepwise":
+        return setup_treemap(torch, P, w, "stored", stepwise=True), step_treemap_stepwise, phases_treemap_stepwise
+    if name == "fused":
+        return setup_tree(torch, P, w, "recompute"), step_tree, phases_tree
+    return setup_treemap(torch, P, w, "recompute"), step_treemap, phases_treemap
+
+
+def run_legs(torch, P, steps, warmup):
+    from workloads import WORKLOADS
+    w = WORKLOADS["many_small"]()
+    legs = {}
+    for name, form, key, desc in LEGS:
+        log("leg %s: setup" % name)
+        S, step, phases = leg_setup(name, torch, P, w)
+        ph, ms, phase_ms = time_workload(torch, P, S, step, phases, steps, warmup)
+        n, K = S["n"], S["K"]
+        byts = sum(p[3] for p in ph)
+        breakdown, roof = summarize(ph, ms, phase_ms, n, K, key)
+        legs[name] = {"form": form, "step": desc, "trajectory": trajectory_label(S), "n_params": n, "leaves": w.nseg,
+                      "K": K, "ms_per_step": round(ms, 4), "G_params_per_s": round(n * K / (ms * 1e-3) / 1e9, 2),
+                      "bytes_per_elem": round(byts / n, 3), "launches_per_step": sum(p[2] for p in ph),
+                      "achieved_GBps": round(byts / (ms * 1e-3) / 1e9, 1),
+                      "hbm_frac": round(byts / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                      "phases": breakdown, "dominant": roof}
+        log("leg %s: %.4f ms/step, %.1f G params/s" % (name, ms, legs[name]["G_params_per_s"]))
+        del S
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return legs
+
+
+WORKLOAD_STEP = {
+    "many_small_stepwise": "flatten p + K grads -> K single-step Adam fwd launches -> K single-step Adam bwd launches "
+                           "-> unflatten p_K + K dg",
+    "flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",
+    "flat_1b_zero_mv": "one Adam fwd + one Adam bwd (count 100, zero mu/nu cotangents: the first backward step of an "
+                       "unrolled loop)",
+    "adam_vs_torch": "one Adam fwd + one Adam bwd (count 100, all cotangents); the same step through torch's "
+                     "differentiable functional Adam and autograd, timed beside it over a size sweep",
+    "many_small_treemap": "leaf-direct K-step Adam fwd -> K-step Adam bwd (no flatten)",
+    "sgd_flat": "one SGD fwd + one SGD bwd on the flat buffer",
+    "rmsprop_flat": "one RMSProp fwd + one RMSProp bwd on the flat buffer",
+    "sgd_treemap": "leaf-direct SGD fwd -> SGD bwd (no flatten)",
+    "rmsprop_treemap": "leaf-direct RMSProp fwd -> RMSProp bwd (no flatten)",
+    "es_resnet18": "perturb theta into 2N points -> ES estimate from N given loss weights",
+}
 
 
 def main():
@@ -693,13 +999,15 @@ def main():
                        "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
                        "es_resnet18": "resnet18_k1", "flat_1b_zero_mv": "flat_1b",
                        "many_small_stepwise": "many_small"}.get(a.workload, a.workload)]()
+    log("workload %s: setup" % a.workload)
+    flat = a.workload in ("flat_1b", "adam_vs_torch", "flat_1b_zero_mv")
     if a.workload == "es_resnet18":
         S, step, phases = setup_es(torch, P, w), step_es, phases_es
     elif a.workload in ("sgd_treemap", "rmsprop_treemap"):
         S, step, phases = setup_optim_tree(torch, P, a.workload.split("_")[0], w), step_optim_tree, phases_optim_tree
     elif a.workload in ("sgd_flat", "rmsprop_flat"):
         S, step, phases = setup_optim(torch, P, a.workload.split("_")[0]), step_optim, phases_optim
-    elif a.workload in ("flat_1b", "adam_vs_torch", "flat_1b_zero_mv"):
+    elif flat:
         S, step, phases = setup_flat_1b(torch, P, w, a.workload == "flat_1b_zero_mv"), step_flat_1b, phases_flat_1b
     elif a.workload == "many_small_stepwise":
         S, step, phases = setup_stepwise(torch, P, w), step_stepwise, phases_stepwise
@@ -707,8 +1015,6 @@ def main():
         S, step, phases = setup_treemap(torch, P, w, a.trajectory), step_treemap, phases_treemap
     else:
         S, step, phases = setup_tree(torch, P, w, a.trajectory), step_tree, phases_tree
-    ph = phases(S)
-    nph = len(ph)
     torch.cuda.synchronize()
 
     # a plain copy of known size, outside the timed region: the calibration
@@ -727,120 +1033,72 @@ def main():
     copy_gbs = 2 * cal_src.numel() * 4 * COPY_REPS / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del cal_src, cal_dst
 
-    for _ in range(a.warmup):
-        step(P, S)
-    torch.cuda.synchronize()
-
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    phase_ms = None
-    if a.graph:
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            step(P, S)
-        torch.cuda.current_stream().wait_stream(side)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            step(P, S)
-        graph.replay()
-        torch.cuda.synchronize()
-        t_start.record()
-        for s in range(a.steps):
-            graph.replay()
-        t_end.record()
-        torch.cuda.synchronize()
-    else:
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)] for _ in range(a.steps)]
-        torch.cuda.synchronize()
-        t_start.record()
-        for s in range(a.steps):
-            step(P, S, evs[s])
-        t_end.record()
-        torch.cuda.synchronize()
-        phase_ms = [sum(e[i].elapsed_time(e[i + 1]) for e in evs) / a.steps for i in range(nph)]
-    total_ms = t_start.elapsed_time(t_end)
-    ms_step = total_ms / a.steps
-
+    log("workload %s: timing %d steps" % (a.workload, a.steps))
+    ph, ms_step, phase_ms = time_workload(torch, P, S, step, phases, a.steps, a.warmup, a.graph)
     n, K = S["n"], S["K"]
     bytes_step = sum(p[3] for p in ph)
     value = n * K / (ms_step * 1e-3)
     gbs = bytes_step / (ms_step * 1e-3) / 1e9
-    breakdown, roofline = {}, None
-    if phase_ms is not None:
-        for (name, kern, launches, byts), t in zip(ph, phase_ms):
-            breakdown[name] = {"ms": round(t, 4), "launches": launches,
-                               "GB/s": round(byts / (t * 1e-3) / 1e9, 1),
-                               "frac": round(byts / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-            if "fwd" in name or "bwd" in name:  # parameter-steps per second of this phase alone
-                breakdown[name]["G_params_per_s"] = round(n * K / (t * 1e-3) / 1e9, 2)
-        dom = max(range(nph), key=lambda i: phase_ms[i])
-        dname, dkern, dlaunch, dbytes = ph[dom]
-        avg_launch_s = phase_ms[dom] * 1e-3 / dlaunch
-        per_launch_bytes = dbytes / dlaunch
-        achieved = per_launch_bytes / avg_launch_s / 1e9
-        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": traffic_from_profile(dkern, a.workload, per_launch_bytes),
-                    "kernel": dkern, "bytes_per_launch": int(per_launch_bytes),
-                    "avg_launch_us": round(avg_launch_s * 1e6, 2)}
+    breakdown, roofline = summarize(ph, ms_step, phase_ms, n, K, a.workload)
+    log("workload %s: %.4f ms/step, %.4g params/s" % (a.workload, ms_step, value))
+    place = placement(S, ["p", "g", "m", "v", "dP", "dM", "dV", "po", "mo", "vo", "dg", "dm", "dv"]) if flat else None
 
-    cpu = None
-    if not a.no_cpu_baseline and a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap",
-                                                    "rmsprop_treemap", "es_resnet18", "adam_vs_torch",
-                                                    "flat_1b_zero_mv", "many_small_stepwise"):
-        cpu = (cpu_baseline_flat_1b if a.workload == "flat_1b" else cpu_baseline_tree)(w, a.cpu_seconds)
-        cpu["value"] = float("%.4g" % cpu["value"])
+    legs = None
+    if a.workload == "flat_1b" and not a.no_legs:
+        legs = run_legs(torch, P, a.steps, a.warmup)
 
+    cpu, parity = None, None
+    if not a.no_cpu_baseline:
+        if a.workload in ("flat_1b", "flat_1b_zero_mv"):
+            cpu = oracle_time_flat(torch, S, progress=log)
+            parity = oracle_check_flat(torch, S, progress=log)
+        elif a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
+                                "es_resnet18", "adam_vs_torch", "many_small_stepwise"):
+            cpu = cpu_baseline_tree(w, a.cpu_seconds)
+            cpu["value"] = float("%.4g" % cpu["value"])
+
+    desc = {
+        "many_small_treemap": w.description.replace(
+            "pack -> K=%d unrolled Adam fwd+bwd -> unpack" % K,
+            "leaf-direct K=%d unrolled Adam fwd+bwd (no pack/unpack)" % K),
+        "sgd_flat": "flat fp32 buffer, n=%d, one Nesterov SGD-momentum fwd + bwd" % n,
+        "rmsprop_flat": "flat fp32 buffer, n=%d, one RMSProp-momentum fwd + bwd" % n,
+        "sgd_treemap": "many-small-tensor tree (20000 leaves, n=%d), one leaf-direct Nesterov SGD-momentum fwd + bwd"
+                       % n,
+        "rmsprop_treemap": "many-small-tensor tree (20000 leaves, n=%d), one leaf-direct RMSProp-momentum fwd + bwd"
+                           % n,
+        "es_resnet18": "ES gradient estimate for n=%d (ResNet-18 size), 64 antithetic samples" % n,
+    }.get(a.workload, w.description)
     out = {
         "metric": METRIC, "value": float("%.6g" % value), "unit": "params/s", "n_gpus": 1,
         "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": {
-                       "many_small_treemap": w.description.replace(
-                           "pack -> K=%d unrolled Adam fwd+bwd -> unpack" % K,
-                           "leaf-direct K=%d unrolled Adam fwd+bwd (no pack/unpack)" % K),
-                       "sgd_flat": "flat fp32 buffer, n=%d, one Nesterov SGD-momentum fwd + bwd" % n,
-                       "rmsprop_flat": "flat fp32 buffer, n=%d, one RMSProp-momentum fwd + bwd" % n,
-                       "sgd_treemap": "many-small-tensor tree (20000 leaves, n=%d), one leaf-direct Nesterov "
-                                      "SGD-momentum fwd + bwd" % n,
-                       "rmsprop_treemap": "many-small-tensor tree (20000 leaves, n=%d), one leaf-direct "
-                                          "RMSProp-momentum fwd + bwd" % n,
-                       "es_resnet18": "ES gradient estimate for n=%d (ResNet-18 size), 64 antithetic samples" % n,
-                   }.get(a.workload, w.description),
-                   "n_params": n, "leaves": w.nseg, "K": K,
-                   "step": {"flat_1b": "one Adam fwd + one Adam bwd (count 100, all cotangents)",
-                            "many_small_stepwise": "flatten p + K grads -> K single-step Adam fwd launches -> K "
-                                                   "single-step Adam bwd launches -> unflatten p_K + K dg",
-                            "flat_1b_zero_mv": "one Adam fwd + one Adam bwd (count 100, zero mu/nu cotangents: "
-                                               "the first backward step of an unrolled loop)",
-                            "adam_vs_torch": "one Adam fwd + one Adam bwd (count 100, all cotangents); the same step "
-                                             "through torch's differentiable functional Adam and autograd, timed "
-                                             "beside it over a size sweep",
-                            "many_small_treemap": "leaf-direct K-step Adam fwd -> K-step Adam bwd (no flatten)",
-                            "sgd_flat": "one SGD fwd + one SGD bwd on the flat buffer",
-                            "rmsprop_flat": "one RMSProp fwd + one RMSProp bwd on the flat buffer",
-                            "sgd_treemap": "leaf-direct SGD fwd -> SGD bwd (no flatten)",
-                            "rmsprop_treemap": "leaf-direct RMSProp fwd -> RMSProp bwd (no flatten)",
-                            "es_resnet18": "perturb theta into 2N points -> ES estimate from N given loss weights"}.get(
-                                a.workload,
-                                "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd -> unflatten p_K + K dg"),
+        "config": {"workload": desc, "n_params": n, "leaves": w.nseg, "K": K,
+                   "step": WORKLOAD_STEP.get(a.workload, "flatten p + K grads -> K-step Adam fwd -> K-step Adam bwd "
+                                                         "-> unflatten p_K + K dg"),
                    "launch": "hip graph replay" if a.graph else "eager", "parallelism": "single GPU",
-                   **({"trajectory": {"recompute": "final moment state stored (and, for K > %d, evenly spaced ones "
-                                                   "so that no recompute run exceeds %d steps); the VJP recomputes "
-                                                   "the rest" % (REMAT_SPAN, REMAT_SPAN),
-                                      "stored": "every moment state stored"}[a.trajectory]}
-                      if "stored" in S else {})},
+                   **({"trajectory": trajectory_label(S)} if "stored" in S else {})},
         "us_per_step": round(ms_step * 1e3, 2),
         "achieved_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "bytes_per_elem": round(bytes_step / n, 3),
         "d2d_copy_GBps": round(copy_gbs, 1), "frac_of_d2d_copy": round(gbs / copy_gbs, 4),
         "bytes_per_step": int(bytes_step), "phases": breakdown,
         "roofline": roofline, "cpu_baseline": cpu,
-        "kernel_src_sha": kernel_source_sha(),
     }
+    if parity is not None:
+        out["oracle_parity"] = parity
+    if legs is not None:
+        out["legs"] = legs
+    if place is not None:
+        out["placement"] = place
+    out["kernel_src_sha"] = kernel_source_sha()
     if a.workload == "adam_vs_torch":
         out["vs_torch_op_by_op"] = torch_op_by_op_sweep(torch, P, VS_TORCH_SIZES, max(a.steps, 10))
     print(json.dumps(out), flush=True)
+    if parity is not None and parity["failures"]:
+        sys.stderr.write("bench.py: %d output elements differ from the oracle beyond the bars; first: %s\n"
+                         % (parity["failures"], parity["first_failure"]))
+        sys.exit(3)
 
 
 if __name__ == "__main__":

@@ -21,7 +21,9 @@ class ConvNet(torch.nn.Module):
     """4 x [conv3x3 (+ bias), BN (batch statistics) scale/shift, ReLU, 2x2 max-pool], linear.
 
     With conv_bias the biases sit in front of batch normalisation, which removes
-    them: their gradient is exactly zero, the 0/0 point of Adam's VJP."""
+    them: their gradient is zero in exact arithmetic and at rounding level in
+    fp32 (some elements exactly zero), the 0/0 point of Adam's VJP and its
+    neighbourhood."""
 
     def __init__(self, width=64, ways=5, conv_bias=True):
         super().__init__()
@@ -138,11 +140,104 @@ def test_maml_meta_gradient_through_fused_adam(K):
 
 
 def test_maml_zero_gradient_biases_stay_finite():
-    # Conv biases in front of batch normalisation have an exactly zero
-    # gradient, so v' = 0 at step 1: the explicit 0/0 case of the fused VJP
-    # gives finite meta-gradients (an op-by-op sqrt backward gives 0 * inf).
+    # Conv biases in front of batch normalisation have a gradient that is zero
+    # up to rounding, often exactly, so v' = 0 at step 1: the explicit 0/0
+    # case of the fused VJP gives finite meta-gradients (an op-by-op sqrt
+    # backward gives 0 * inf).
     torch.manual_seed(1)
     init = {n: p.detach().clone() for n, p in ConvNet(conv_bias=True).named_parameters()}
     ours, out_ours = _meta_grad_ours(init, _task(6), 2, "cuda", conv_bias=True)
     assert np.isfinite(out_ours)
     assert all(torch.isfinite(g).all() for g in ours)
+
+
+def _recording_adam_tree_fn(log):
+    """AdamTreeFn that also records, per call, what its kernels were given and
+    what they returned: forward (count, p, g, m, v -> p', m', v') and backward
+    (saved g, m, v and the incoming cotangents -> dp, dg, dm, dv), as fp64
+    numpy arrays over the concatenated leaves."""
+    import paper_2211_06934_amd as P
+    base = P.autograd.AdamTreeFn
+    cat = lambda ts: np.concatenate([t.detach().reshape(-1).double().cpu().numpy() for t in ts])  # noqa: E731
+
+    class Rec(base):
+        @staticmethod
+        def forward(ctx, table, count, hyper, *leaves):
+            out = base.forward(ctx, table, count, hyper, *leaves)
+            S = len(leaves) // 4
+            torch.cuda.synchronize()
+            log.append(dict(kind="fwd", count=count, hyper=hyper,
+                            inp=[cat(leaves[i * S:(i + 1) * S]) for i in range(4)],
+                            out=[cat(out[i * S:(i + 1) * S]) for i in range(3)]))
+            return out
+
+        @staticmethod
+        def backward(ctx, *cots):
+            res = base.backward(ctx, *cots)
+            S = ctx.S
+            saved = ctx.saved_tensors
+            torch.cuda.synchronize()
+            zero_or = lambda grp, like: [torch.zeros_like(x) if c is None else c for c, x in zip(grp, like)]  # noqa
+            log.append(dict(kind="bwd", count=ctx.count, hyper=ctx.hyper,
+                            saved=[cat(saved[i * S:(i + 1) * S]) for i in range(3)],
+                            cots=[cat(zero_or(cots[i * S:(i + 1) * S], saved[:S])) for i in range(3)],
+                            res=[cat(res[3 + i * S:3 + (i + 1) * S]) for i in range(4)]))
+            return res
+
+    return Rec
+
+
+@pytest.mark.parametrize("K,conv_bias", [(1, False), (3, False), (2, True)])
+def test_maml_fused_steps_match_oracle_inside_the_loop(K, conv_bias, monkeypatch):
+    # Every fused step the real MAML loop runs -- warm moments after step 1,
+    # cotangents that carry the model's Hessian-vector products into the
+    # earlier steps, and (conv_bias) zero-gradient leaves at the 0/0 point
+    # mixed with live ones -- checked element by element against the oracle
+    # on the inputs that step actually received: 1e-5 of the term scale for
+    # the forward, 1e-4 for the VJP, and the params cotangent passed through
+    # bit for bit.
+    import oracle
+    import paper_2211_06934_amd as P
+    from tests.support import BWD_RTOL, FWD_RTOL, assert_mag_close
+    log = []
+    monkeypatch.setattr(P.autograd, "AdamTreeFn", _recording_adam_tree_fn(log))
+    torch.manual_seed(2 + K)
+    init = {n: p.detach().clone() for n, p in ConvNet(conv_bias=conv_bias).named_parameters()}
+    grads, outer = _meta_grad_ours(init, _task(7 + K), K, "cuda", conv_bias=conv_bias)
+    assert np.isfinite(outer) and all(torch.isfinite(g).all() for g in grads)
+    fw = [r for r in log if r["kind"] == "fwd"]
+    bw = [r for r in log if r["kind"] == "bwd"]
+    assert [r["count"] for r in fw] == list(range(K)) and sorted(r["count"] for r in bw) == list(range(K))
+    zero_g, tiny_g = 0, 0
+    for r in fw:
+        h = r["hyper"]
+        hy = (r["count"], h.lr, h.b1, h.b2, h.eps, h.eps_root)
+        p, g, m, v = r["inp"]
+        ref = oracle.adam_fwd(p, g, m, v, *hy)
+        mag = oracle.adam_fwd_mag(p, g, m, v, *hy)
+        for name, got, x, mg in zip(("p'", "m'", "v'"), r["out"], ref, mag):
+            assert_mag_close(got, x, mg, FWD_RTOL, "step %d %s" % (r["count"], name))
+        zero_g += int(np.sum(g == 0.0))
+        tiny_g += int(np.sum(np.abs(g) < 1e-8))  # s at or below eps: the neighbourhood of the 0/0 point
+    for r in bw:
+        h = r["hyper"]
+        hy = (r["count"], h.lr, h.b1, h.b2, h.eps, h.eps_root)
+        g, m, v = r["saved"]
+        dP, dM, dV = r["cots"]
+        ref = oracle.adam_bwd(dP, dM, dV, g, m, v, *hy)
+        mag = oracle.adam_bwd_mag(dP, dM, dV, g, m, v, *hy)
+        assert np.array_equal(r["res"][0], dP), "params cotangent is the identity"
+        for name, got, x, mg in zip(("dg", "dm", "dv"), r["res"][1:], ref[1:], mag):
+            assert_mag_close(got, x, mg, BWD_RTOL, "VJP step %d %s" % (r["count"], name))
+    print("K=%d conv_bias=%s: %d gradient elements exactly 0, %d below 1e-8" % (K, conv_bias, zero_g, tiny_g))
+    if conv_bias:
+        # the biases in front of batch normalisation have a gradient that is
+        # zero in exact arithmetic and at rounding level in fp32: the loop
+        # reaches the 0/0 point itself (exact zeros) and its neighbourhood
+        assert tiny_g >= 1, (zero_g, tiny_g)
+    # the cotangents of the earlier steps are not just the outer gradient:
+    # they carry the model's second-order terms
+    if K > 1:
+        last = [r for r in bw if r["count"] == K - 1][0]
+        first = [r for r in bw if r["count"] == 0][0]
+        assert not np.allclose(first["cots"][0], last["cots"][0])
