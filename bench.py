@@ -32,7 +32,10 @@ Other workloads (--workload), each printing its own line:
   many_small_stepwise      the stepwise pass alone
   sgd_flat | rmsprop_flat | sgd_treemap | rmsprop_treemap
                            one fwd + bwd of the other fused optimizers
-  es_resnet18              ES perturb + estimate at the ResNet-18 size
+  small_trees              the small trees in three forms (pack + fused + unpack, leaf-direct
+                           fused, leaf-direct one launch per step), HIP graph replay
+  es_resnet18 [_noise]     ES perturb + estimate at the ResNet-18 size, noise generated in
+                           the kernels (_noise: read from an N x n array)
   adam_vs_torch            the interior Adam step at 10^8, plus the same step in
                            torch ops over a size sweep (field vs_torch_op_by_op)
 --graph replays one captured step as a HIP graph (the small trees are
@@ -128,7 +131,8 @@ def parse():
     ap.add_argument("--workload", default="flat_1b",
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
                              "many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
-                             "es_resnet18", "adam_vs_torch", "flat_1b_zero_mv", "many_small_stepwise"])
+                             "es_resnet18", "es_resnet18_noise", "adam_vs_torch", "flat_1b_zero_mv",
+                             "many_small_stepwise", "small_trees"])
     ap.add_argument("--trajectory", choices=["stored", "recompute"], default="recompute",
                     help="K-step driver: store every moment state for the backward, or store only the final one "
                          "(and every %d-th) and let the backward recompute the rest in registers" % REMAT_SPAN)
@@ -157,6 +161,8 @@ KERNEL_SOURCES = {  # the sources each kernel family is built from
     "rmsprop_fwd": ("optim.hip", "optim_ops.hpp", "adam_math.hpp", "common.hpp"),
     "rmsprop_bwd": ("optim.hip", "optim_ops.hpp", "adam_math.hpp", "common.hpp"),
     "es_perturb": ("es.hip", "adam_math.hpp", "common.hpp"), "es_estimate": ("es.hip", "adam_math.hpp", "common.hpp"),
+    "es_perturb_gaussian": ("es.hip", "adam_math.hpp", "common.hpp"),
+    "es_estimate_gaussian": ("es.hip", "adam_math.hpp", "common.hpp"),
     "sgd_fwd_tree": ("treemap.hip", "optim_ops.hpp", "adam_math.hpp", "segtable.hpp", "common.hpp"),
     "sgd_bwd_tree": ("treemap.hip", "optim_ops.hpp", "adam_math.hpp", "segtable.hpp", "common.hpp"),
     "rmsprop_fwd_tree": ("treemap.hip", "optim_ops.hpp", "adam_math.hpp", "segtable.hpp", "common.hpp"),
@@ -587,35 +593,53 @@ def phases_optim(S):
     return [("rmsprop_fwd", "rmsprop_fwd", 1, 28 * n), ("rmsprop_bwd", "rmsprop_bwd", 1, 32 * n)]
 
 
-def setup_es(torch, P, w):
-    """Zero-order (ES) estimation for the ResNet-18 parameter count: 64
-    antithetic noise rows, the perturbed points, and the weighted reduction
-    (the weights stand in for the caller's evaluations)."""
+def setup_es(torch, P, w, noise_input=False):
+    """Zero-order (ES) estimation for the ResNet-18 parameter count with 64
+    antithetic samples: the perturbed points and the estimate from the
+    evaluations (seeded values stand in for the caller's f).  By default the
+    Gaussian noise is generated inside both kernels from a seed; noise_input
+    takes it from an N x n array instead (a caller's own sampler)."""
     from workloads import torch_normal
     n, N, dev = w.n, 64, "cuda"
-    S = dict(K=1, n=n, N=N, sigma=0.05, theta=torch_normal(n, 0.05, 401, dev),
-             noise=torch_normal(N * n, 1.0, 402, dev).reshape(N, n),
-             pts=torch.empty(2 * N, n, device=dev), w=torch_normal(N, 1.0, 403, dev),
-             grad=torch.empty(n, device=dev))
+    S = dict(K=1, n=n, N=N, sigma=0.05, seed=20221112, noise_input=noise_input,
+             theta=torch_normal(n, 0.05, 401, dev), pts=torch.empty(2 * N, n, device=dev),
+             fvals=torch_normal(2 * N, 1.0, 403, dev), grad=torch.empty(n, device=dev))
+    if noise_input:
+        S["noise"] = torch_normal(N * n, 1.0, 402, dev).reshape(N, n)
+        S["w"] = torch.empty(N, device=dev)
     return S
 
 
 def step_es(P, S, ev=None):
+    N, sigma = S["N"], S["sigma"]
     if ev:
         ev[0].record()
-    P.es_perturb(S["theta"], S["noise"], S["sigma"], True, S["pts"])
+    if S["noise_input"]:
+        P.es_perturb(S["theta"], S["noise"], sigma, True, S["pts"])
+    else:
+        P.es_perturb_gaussian(S["theta"], N, S["seed"], sigma, True, S["pts"])
     if ev:
         ev[1].record()
-    P.es_estimate(S["noise"], S["w"], 1.0 / (2 * S["N"] * S["sigma"]), S["grad"])
+    if S["noise_input"]:
+        P.es_weights(S["fvals"], "antithetic", N, sigma, S["w"])
+        P.es_estimate(S["noise"], S["w"], 1.0, S["grad"])
+    else:
+        P.es_estimate_gaussian(S["fvals"], "antithetic", N, S["seed"], sigma, S["grad"])
     if ev:
         ev[2].record()
 
 
 def phases_es(S):
     n, N = S["n"], S["N"]
-    # perturb: theta once + N noise rows in, 2N points out; estimate: N rows in, grad out
-    return [("es_perturb", "es_perturb", 1, 4 * n + 4 * N * n + 8 * N * n),
-            ("es_estimate", "es_estimate", 1, 4 * N * n + 4 * n)]
+    if S["noise_input"]:
+        # perturb: theta once + N noise rows in, 2N points out; estimate: 2N
+        # evaluations and N noise rows in, grad out (weights: 12N, negligible)
+        return [("es_perturb", "es_perturb", 1, 4 * n + 4 * N * n + 8 * N * n),
+                ("es_estimate", "es_estimate", 2, 4 * N * n + 4 * n + 20 * N)]
+    # noise generated in the kernels: perturb reads theta and writes 2N
+    # points; the estimate reads the 2N evaluations and writes grad
+    return [("es_perturb", "es_perturb_gaussian", 1, 4 * n + 8 * N * n),
+            ("es_estimate", "es_estimate_gaussian", 1, 8 * N + 4 * n)]
 
 
 def phases_flat_1b(S):
@@ -962,6 +986,40 @@ def run_legs(torch, P, steps, warmup):
     return legs
 
 
+SMALL_TREES = ("tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10")
+SMALL_FORMS = (
+    ("pack_fused_unpack", "flatten p + K grads -> fused K-step fwd -> fused K-step VJP -> unflatten p_K + K dg"),
+    ("leaf_direct_fused", "leaf-direct fused K-step fwd -> fused K-step VJP (no pack/unpack)"),
+    ("leaf_direct_stepwise", "leaf-direct single-step fwd x K -> single-step VJP x K (every state stored)"),
+)
+
+
+def small_trees(torch, P, steps, warmup):
+    """The small trees (launch-bound) in three forms, each captured in a HIP
+    graph and replayed: microseconds per step and launches per step."""
+    from workloads import WORKLOADS
+    table = {}
+    for wname in SMALL_TREES:
+        w = WORKLOADS[wname]()
+        row = {"n_params": w.n, "leaves": w.nseg, "K": w.K}
+        for form, _ in SMALL_FORMS:
+            if form == "pack_fused_unpack":
+                S, step, phases = setup_tree(torch, P, w, "recompute"), step_tree, phases_tree
+            elif form == "leaf_direct_fused":
+                S, step, phases = setup_treemap(torch, P, w, "recompute"), step_treemap, phases_treemap
+            else:
+                S, step, phases = (setup_treemap(torch, P, w, "stored", stepwise=True), step_treemap_stepwise,
+                                   phases_treemap_stepwise)
+            ph, ms, _ = time_workload(torch, P, S, step, phases, steps, warmup, graph=True)
+            row[form] = {"us_per_step": round(ms * 1e3, 2), "launches_per_step": sum(p[2] for p in ph),
+                         "G_params_per_s": round(w.n * w.K / (ms * 1e-3) / 1e9, 3)}
+            log("%s %s: %.2f us/step" % (wname, form, ms * 1e3))
+            del S
+            torch.cuda.synchronize()
+        table[wname] = row
+    return table
+
+
 WORKLOAD_STEP = {
     "many_small_stepwise": "flatten p + K grads -> K single-step Adam fwd launches -> K single-step Adam bwd launches "
                            "-> unflatten p_K + K dg",
@@ -975,7 +1033,10 @@ WORKLOAD_STEP = {
     "rmsprop_flat": "one RMSProp fwd + one RMSProp bwd on the flat buffer",
     "sgd_treemap": "leaf-direct SGD fwd -> SGD bwd (no flatten)",
     "rmsprop_treemap": "leaf-direct RMSProp fwd -> RMSProp bwd (no flatten)",
-    "es_resnet18": "perturb theta into 2N points -> ES estimate from N given loss weights",
+    "es_resnet18": "perturb theta into 2N points -> ES estimate from the 2N evaluations (antithetic), the noise "
+                   "regenerated in both kernels",
+    "es_resnet18_noise": "perturb theta into 2N points -> weights from the 2N evaluations -> ES estimate, the noise "
+                         "read from an N x n array",
 }
 
 
@@ -997,12 +1058,28 @@ def main():
     else:
         w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
                        "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
-                       "es_resnet18": "resnet18_k1", "flat_1b_zero_mv": "flat_1b",
+                       "es_resnet18": "resnet18_k1", "es_resnet18_noise": "resnet18_k1", "flat_1b_zero_mv": "flat_1b",
                        "many_small_stepwise": "many_small"}.get(a.workload, a.workload)]()
+    if a.workload == "small_trees":
+        table = small_trees(torch, P, max(a.steps, 100), max(a.warmup, 5))
+        t = table["tiny_mlp"]["leaf_direct_fused"]
+        w = WORKLOADS["tiny_mlp"]()
+        print(json.dumps({
+            "metric": METRIC, "value": float("%.6g" % (w.n * w.K / (t["us_per_step"] * 1e-6))), "unit": "params/s",
+            "n_gpus": 1, "steps": max(a.steps, 100), "warmup": max(a.warmup, 5),
+            "ms_per_step": round(t["us_per_step"] * 1e-3, 6), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": "the small trees (tiny MLP K=5, conv-net x32 K=5, ResNet-18 K=1 and K=10) in three "
+                                   "forms, HIP graph replay; value: tiny MLP leaf-direct fused",
+                       "launch": "hip graph replay", "parallelism": "single GPU",
+                       "forms": {f: d for f, d in SMALL_FORMS}},
+            "small_trees": table, "roofline": None, "cpu_baseline": None,
+            "kernel_src_sha": kernel_source_sha()}), flush=True)
+        return
     log("workload %s: setup" % a.workload)
     flat = a.workload in ("flat_1b", "adam_vs_torch", "flat_1b_zero_mv")
-    if a.workload == "es_resnet18":
-        S, step, phases = setup_es(torch, P, w), step_es, phases_es
+    if a.workload in ("es_resnet18", "es_resnet18_noise"):
+        S, step, phases = setup_es(torch, P, w, a.workload == "es_resnet18_noise"), step_es, phases_es
     elif a.workload in ("sgd_treemap", "rmsprop_treemap"):
         S, step, phases = setup_optim_tree(torch, P, a.workload.split("_")[0], w), step_optim_tree, phases_optim_tree
     elif a.workload in ("sgd_flat", "rmsprop_flat"):
@@ -1053,7 +1130,7 @@ def main():
             cpu = oracle_time_flat(torch, S, progress=log)
             parity = oracle_check_flat(torch, S, progress=log)
         elif a.workload not in ("many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
-                                "es_resnet18", "adam_vs_torch", "many_small_stepwise"):
+                                "es_resnet18", "es_resnet18_noise", "adam_vs_torch", "many_small_stepwise"):
             cpu = cpu_baseline_tree(w, a.cpu_seconds)
             cpu["value"] = float("%.4g" % cpu["value"])
 
@@ -1067,7 +1144,10 @@ def main():
                        % n,
         "rmsprop_treemap": "many-small-tensor tree (20000 leaves, n=%d), one leaf-direct RMSProp-momentum fwd + bwd"
                            % n,
-        "es_resnet18": "ES gradient estimate for n=%d (ResNet-18 size), 64 antithetic samples" % n,
+        "es_resnet18": "ES gradient estimate for n=%d (ResNet-18 size), 64 antithetic samples, Gaussian noise "
+                       "generated in the kernels" % n,
+        "es_resnet18_noise": "ES gradient estimate for n=%d (ResNet-18 size), 64 antithetic samples, noise read "
+                             "from an N x n array" % n,
     }.get(a.workload, w.description)
     out = {
         "metric": METRIC, "value": float("%.6g" % value), "unit": "params/s", "n_gpus": 1,

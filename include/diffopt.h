@@ -434,6 +434,58 @@ int diffopt_es_estimate(const float* noise, const float* weights,
                         int64_t num_samples, int64_t n, double scale,
                         float* grad, void* stream);
 
+/* The same two steps with the Gaussian noise generated inside the kernels
+ * (Sec. 2.2; Listing 3 makes the noise sampler part of the estimator): no
+ * noise array exists.  z_ij, for sample i < num_samples and parameter
+ * j < n, is a pure function of (seed, i, j):
+ *   slot   = with q = j mod 512: block c = 64 (j / 512) + (q mod 256) / 4,
+ *            word w = 2 (q / 256) + (q mod 4) / 2, and the cosine normal for
+ *            even q, the sine one for odd q (so block c covers two runs of
+ *            four parameters 256 apart, and 64 consecutive blocks fill two
+ *            contiguous 1 KiB runs);
+ *   block  = Philox-4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011) of the
+ *            counter (c, i, 0, 0) under the key (seed, 0): four 64-bit
+ *            words;
+ *   word   = word w of the block, split into its low and high 32 bits lo, hi;
+ *   u1     = (floor(lo / 2^8) + 1) 2^-24 in (0, 1], u2 = floor(hi / 2^8) 2^-24
+ *            in [0, 1);
+ *   z_ij   = sqrt(-2 ln u1) cos(2 pi u2) for even q, sqrt(-2 ln u1)
+ *            sin(2 pi u2) for odd q (Box and Muller, 1958), computed in fp32
+ *            (within a few fp32 ulp of the exact value times 1 + |z|).
+ * The same seed gives the same z in both calls, and in any launch shape.
+ *
+ * es_perturb_gaussian: out as for diffopt_es_perturb ([N][n], or [2N][n]
+ *   with antithetic != 0); num_samples <= 65,535 x 8.  n % 4 == 0 with
+ *   16-byte aligned pointers takes 128-bit accesses, anything else an element
+ *   path with the same result.
+ * es_estimate_gaussian: grad_j = scale * sum_i w_i z_ij, accumulated in
+ *   sample order in fp32, with the weights and scale formed in the kernel
+ *   from the caller's evaluations `fvals` (a DEVICE array):
+ *     method 0, plain:      w_i = f_i,            scale = 1/(N s), fvals [N]
+ *     method 1, baseline:   w_i = f_i - *f0,      scale = 1/(N s), fvals [N],
+ *                           f0 a DEVICE pointer to f(theta)
+ *     method 2, antithetic: w_i = f_i - f_{N+i},  scale = 1/(2 N s), fvals [2N]
+ *                           (the evaluations of the rows es_perturb_gaussian
+ *                           wrote, in order)
+ *   scale is formed in fp64 and rounded once.  sigma must be finite and
+ *   nonzero; num_samples == 0 writes zeros.                              */
+int diffopt_es_perturb_gaussian(const float* params, int64_t n,
+                                int64_t num_samples, uint64_t seed,
+                                double sigma, int32_t antithetic, float* out,
+                                void* stream);
+int diffopt_es_estimate_gaussian(const float* fvals, const float* f0,
+                                 int64_t num_samples, int32_t method,
+                                 int64_t n, uint64_t seed, double sigma,
+                                 float* grad, void* stream);
+
+/* es_weights: weights[i] = scale * w_i, the method's weights and scale as in
+ * diffopt_es_estimate_gaussian, for diffopt_es_estimate with scale 1 (a
+ * caller that draws its own noise, e.g. from another distribution).  DEVICE
+ * arrays; num_samples == 0 is a no-op.                                    */
+int diffopt_es_weights(const float* fvals, const float* f0,
+                       int64_t num_samples, int32_t method, double sigma,
+                       float* weights, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -87,6 +87,10 @@ def _configure(lib):
     lib.oracle_box_muller.restype = None
     lib.oracle_es_gaussian_noise.argtypes = [i64, i64, ctypes.c_uint64, d]
     lib.oracle_es_gaussian_noise.restype = None
+    lib.oracle_es_gaussian_noise_radius.argtypes = [i64, i64, ctypes.c_uint64, d]
+    lib.oracle_es_gaussian_noise_radius.restype = None
+    lib.oracle_es_gaussian_noise_cols.argtypes = [i64, i64, ctypes.POINTER(i64), ctypes.c_uint64, d, d]
+    lib.oracle_es_gaussian_noise_cols.restype = None
     lib.oracle_es_weights.argtypes = [i64, d, f64, i64, f64, d, d]
     lib.oracle_es_weights.restype = None
     return lib
@@ -377,6 +381,23 @@ def es_gaussian_noise(N, n, seed):
     z = np.empty((int(N), int(n)))
     _load().oracle_es_gaussian_noise(int(N), int(n), ctypes.c_uint64(int(seed)), _ptr(z))
     return z
+
+
+def es_gaussian_noise_radius(N, n, seed):
+    """Tolerance scale of each noise element: the Box-Muller radius of its pair."""
+    r = np.empty((int(N), int(n)))
+    _load().oracle_es_gaussian_noise_radius(int(N), int(n), ctypes.c_uint64(int(seed)), _ptr(r))
+    return r
+
+
+def es_gaussian_noise_cols(N, cols, seed):
+    """(z, r) of the noise at the given parameter indices only: [N, len(cols)] each."""
+    cols = np.ascontiguousarray(np.asarray(cols, dtype=np.int64).reshape(-1))
+    z = np.empty((int(N), cols.size))
+    r = np.empty((int(N), cols.size))
+    _load().oracle_es_gaussian_noise_cols(int(N), cols.size, cols.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                          ctypes.c_uint64(int(seed)), _ptr(z), _ptr(r))
+    return z, r
 
 
 def es_weights(fvals, method, sigma, f0=0.0):

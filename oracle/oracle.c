@@ -531,22 +531,42 @@ void oracle_box_muller(uint64_t word, double* za, double* zb) {
 }
 
 /*
- * The noise matrix z (N x n, row-major) for a seed: element j of sample i
- * takes word (j mod 8) / 2 of the Philox block at counter (j / 8, i, 0, 0)
- * under key (seed, 0), through the Box-Muller transform above: za for even
- * j, zb for odd j.  Eight consecutive elements share one block.
+ * Which parameters a Philox block covers.  The parameters are cut into
+ * segments of 512; block c = 64 s + l (segment s, slot l < 64) covers the
+ * four parameters 512 s + 4 l + e and the four parameters 512 s + 256 + 4 l + e
+ * (e < 4): word 2 h + e / 2 of the block (h = 0 for the first four, 1 for the
+ * second) gives parameters with even e its cosine normal and odd e its sine
+ * normal.  (This puts the eight normals of one block into two 16-byte vectors
+ * 1 KiB apart, so 64 consecutive blocks fill two contiguous 1 KiB runs.)
+ * noise_slot maps a parameter index to its block, word and normal.
+ */
+static void noise_slot(int64_t j, uint64_t* block, int* word, int* odd) {
+  int64_t s = j / 512, q = j % 512;
+  *block = (uint64_t)(64 * s + (q % 256) / 4);
+  *word = 2 * (int)(q / 256) + (int)(q % 4) / 2;
+  *odd = (int)(q % 2);
+}
+
+/*
+ * The noise matrix z (N x n, row-major) for a seed: element j of sample i is
+ * the normal noise_slot(j) names in the Philox block at counter
+ * (block, i, 0, 0) under key (seed, 0), through the Box-Muller transform.
  */
 void oracle_es_gaussian_noise(int64_t N, int64_t n, uint64_t seed, double* z) {
   uint64_t key[2] = {seed, 0};
+  int64_t nblocks = 64 * ((n + 511) / 512);
   for (int64_t i = 0; i < N; ++i)
-    for (int64_t b = 0; b * 8 < n; ++b) {
+    for (int64_t b = 0; b < nblocks; ++b) {
       uint64_t ctr[4] = {(uint64_t)b, (uint64_t)i, 0, 0}, out[4];
       oracle_philox4x64_10(ctr, key, out);
-      for (int64_t e = 0; e < 8 && b * 8 + e < n; ++e) {
-        double za, zb;
-        oracle_box_muller(out[e / 2], &za, &zb);
-        z[i * n + b * 8 + e] = (e % 2 == 0) ? za : zb;
-      }
+      for (int h = 0; h < 2; ++h)
+        for (int e = 0; e < 4; ++e) {
+          int64_t j = 512 * (b / 64) + 256 * h + 4 * (b % 64) + e;
+          if (j >= n) continue;
+          double za, zb;
+          oracle_box_muller(out[2 * h + e / 2], &za, &zb);
+          z[i * n + j] = (e % 2 == 0) ? za : zb;
+        }
     }
 }
 
@@ -570,4 +590,43 @@ void oracle_es_weights(int64_t N, const double* f, double f0, int64_t method, do
       w[i] = f[i] - f[N + i];
   }
   *scale = 1.0 / ((method == 2 ? 2.0 : 1.0) * (double)N * sigma);
+}
+
+/* Tolerance scale of each noise element: the radius r = sqrt(-2 ln u1) of
+ * its Box-Muller pair.  z = r cos(a) (or r sin(a)) is the product of r and a
+ * factor of magnitude up to 1 whose rounding is absolute, so r, not |z|,
+ * sizes the error of a computed z. */
+void oracle_es_gaussian_noise_radius(int64_t N, int64_t n, uint64_t seed, double* r) {
+  uint64_t key[2] = {seed, 0};
+  for (int64_t i = 0; i < N; ++i)
+    for (int64_t j = 0; j < n; ++j) {
+      uint64_t block, out[4];
+      int word, odd;
+      noise_slot(j, &block, &word, &odd);
+      uint64_t ctr[4] = {block, (uint64_t)i, 0, 0};
+      oracle_philox4x64_10(ctr, key, out);
+      uint32_t lo = (uint32_t)out[word];
+      r[i * n + j] = sqrt(-2.0 * log(((double)(lo >> 8) + 1.0) * 0x1p-24));
+    }
+}
+
+/* The same noise (and radius) at chosen parameters only: z[i * ncols + c] is
+ * element cols[c] of sample i, by the definition above.  For sampled checks
+ * of large estimates. */
+void oracle_es_gaussian_noise_cols(int64_t N, int64_t ncols, const int64_t* cols, uint64_t seed, double* z,
+                                   double* r) {
+  uint64_t key[2] = {seed, 0};
+  for (int64_t i = 0; i < N; ++i)
+    for (int64_t c = 0; c < ncols; ++c) {
+      uint64_t block, out[4];
+      int word, odd;
+      noise_slot(cols[c], &block, &word, &odd);
+      uint64_t ctr[4] = {block, (uint64_t)i, 0, 0};
+      oracle_philox4x64_10(ctr, key, out);
+      double za, zb;
+      oracle_box_muller(out[word], &za, &zb);
+      z[i * ncols + c] = odd ? zb : za;
+      uint32_t lo = (uint32_t)out[word];
+      r[i * ncols + c] = sqrt(-2.0 * log(((double)(lo >> 8) + 1.0) * 0x1p-24));
+    }
 }

@@ -18,6 +18,7 @@ from .diffopt import (DiffoptError, SegTable, adam_bwd, adam_bwd_tree, adam_fwd,
                       segtable_nseg, segtable_total, tree_flatten, tree_unflatten,
                       tree_flatten_batch, tree_unflatten_batch,
                       sgd_fwd, sgd_bwd, rmsprop_fwd, rmsprop_bwd, es_perturb, es_estimate,
+                      es_perturb_gaussian, es_estimate_gaussian, es_weights,
                       sgd_fwd_tree, sgd_bwd_tree, rmsprop_fwd_tree, rmsprop_bwd_tree)
 from . import tree
 from . import autograd
@@ -29,7 +30,7 @@ __all__ = [
     "adam_unrolled_bwd", "adam_unrolled_fwd", "adam_fwd_tree", "adam_bwd_tree",
     "adam_unrolled_fwd_tree", "adam_unrolled_bwd_tree", "sgd_fwd", "sgd_bwd", "rmsprop_fwd", "rmsprop_bwd",
     "sgd_fwd_tree", "sgd_bwd_tree", "rmsprop_fwd_tree", "rmsprop_bwd_tree",
-    "es_perturb", "es_estimate", "last_error", "segtable_create", "segtable_destroy",
+    "es_perturb", "es_estimate", "es_perturb_gaussian", "es_estimate_gaussian", "es_weights", "last_error", "segtable_create", "segtable_destroy",
     "segtable_nseg", "segtable_total", "tree_flatten", "tree_unflatten", "tree_flatten_batch",
     "tree_unflatten_batch", "AdamFn", "AdamHyper",
     "AdamState", "FlatAdam", "AdamTreeFn", "MetaAdam", "SGDHyper", "SGDTreeFn", "MetaSGD", "RMSPropHyper",

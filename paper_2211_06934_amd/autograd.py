@@ -393,41 +393,59 @@ class MetaRMSProp(_MetaOptimizer):
 
 
 def es_gradient(fn, theta: torch.Tensor, sigma: float, num_samples: int, method: str = "antithetic",
-                generator: torch.Generator = None) -> torch.Tensor:
+                seed: int = None, sample=None) -> torch.Tensor:
     """Zero-order (ES) estimate of the gradient of the Gaussian smoothing of fn
-    at theta (Sec. 2.2): draws N(0, I) noise with the caller's generator,
-    builds the perturbed points with diffopt_es_perturb, evaluates fn on them
-    as one batch (fn maps [M, n] to [M]) and reduces with diffopt_es_estimate.
+    at theta (Sec. 2.2).  fn maps a batch [M, n] to [M] and is evaluated once
+    on all perturbed points (and once on theta for the baseline method).
+
+    By default the N(0, I) noise is generated inside the kernels from `seed`
+    (a 64-bit integer; drawn from torch's CPU generator when None): the
+    perturbed points come from diffopt_es_perturb_gaussian and the estimate
+    from diffopt_es_estimate_gaussian, which forms the method's weights from
+    the evaluations, so no noise array exists.  `sample`, a callable
+    (num_samples, n) -> [num_samples, n] device tensor, draws the noise from
+    another distribution instead (Listing 3's customisable sampler); then the
+    explicit-noise kernels run, with the weights formed by diffopt_es_weights.
     method: "plain", "baseline" (subtract f(theta)) or "antithetic"."""
-    if method not in ("plain", "baseline", "antithetic"):
+    if method not in _d.ES_METHODS:
         raise ValueError("method must be plain, baseline or antithetic")
     theta = theta.detach().contiguous().reshape(-1)
     n = theta.numel()
-    noise = torch.randn(num_samples, n, device=theta.device, dtype=theta.dtype, generator=generator)
     anti = method == "antithetic"
     pts = torch.empty((2 if anti else 1) * num_samples, n, device=theta.device, dtype=theta.dtype)
-    _d.es_perturb(theta, noise, sigma, anti, pts)
+    noise = None
+    if sample is None:
+        if seed is None:
+            seed = int(torch.randint(0, 2 ** 62, (1,)).item())
+        _d.es_perturb_gaussian(theta, num_samples, seed, sigma, anti, pts)
+    else:
+        noise = sample(num_samples, n)
+        if tuple(noise.shape) != (num_samples, n):
+            raise ValueError("sample must return a [num_samples, n] tensor")
+        noise = noise.to(device=theta.device, dtype=theta.dtype).contiguous()
+        _d.es_perturb(theta, noise, sigma, anti, pts)
     with torch.no_grad():
-        fv = fn(pts).reshape(-1).to(theta.dtype)
-        if method == "plain":
-            w, scale = fv, 1.0 / (num_samples * sigma)
-        elif method == "baseline":
-            w, scale = fv - fn(theta.reshape(1, -1)).reshape(()), 1.0 / (num_samples * sigma)
-        else:
-            w, scale = fv[:num_samples] - fv[num_samples:], 1.0 / (2 * num_samples * sigma)
+        fv = fn(pts).reshape(-1).to(theta.dtype).contiguous()
+        f0 = fn(theta.reshape(1, -1)).reshape(1).to(theta.dtype).contiguous() if method == "baseline" else None
     grad = torch.empty_like(theta)
-    _d.es_estimate(noise, w.contiguous(), scale, grad)
+    if noise is None:
+        _d.es_estimate_gaussian(fv, method, num_samples, seed, sigma, grad, f0=f0)
+    else:
+        w = torch.empty(num_samples, device=theta.device, dtype=theta.dtype)
+        _d.es_weights(fv, method, num_samples, sigma, w, f0=f0)
+        _d.es_estimate(noise, w, 1.0, grad)
     return grad
 
 
 class ZeroOrderFn(torch.autograd.Function):
     """y = fn(theta) whose backward is the ES gradient estimate (Sec. 2.2,
-    the zero_order decorator's behaviour): grad_theta = grad_y * estimate."""
+    the zero_order decorator's behaviour): grad_theta = grad_y * estimate.
+    apply(theta, fn, sigma, num_samples, method, seed[, sample])."""
 
     @staticmethod
-    def forward(ctx, theta, fn, sigma, num_samples, method, generator):
+    def forward(ctx, theta, fn, sigma, num_samples, method, seed=None, sample=None):
         ctx.save_for_backward(theta)
-        ctx.cfg = (fn, sigma, num_samples, method, generator)
+        ctx.cfg = (fn, sigma, num_samples, method, seed, sample)
         with torch.no_grad():
             return fn(theta.detach().reshape(1, -1)).reshape(())
 
@@ -435,6 +453,6 @@ class ZeroOrderFn(torch.autograd.Function):
     @once_differentiable
     def backward(ctx, grad_y):
         (theta,) = ctx.saved_tensors
-        fn, sigma, num_samples, method, generator = ctx.cfg
-        g = es_gradient(fn, theta, sigma, num_samples, method, generator).reshape(theta.shape)
-        return grad_y * g, None, None, None, None, None
+        fn, sigma, num_samples, method, seed, sample = ctx.cfg
+        g = es_gradient(fn, theta, sigma, num_samples, method, seed, sample).reshape(theta.shape)
+        return grad_y * g, None, None, None, None, None, None

@@ -174,6 +174,191 @@ __global__ __launch_bounds__(kEB) void es_estimate_scalar(const float* noise, co
   grad[j] = scale * acc;
 }
 
+// ---- Gaussian noise generated in registers -----------------------------------
+//
+// z_ij (sample i, parameter j) is a pure function of (seed, i, j), so the
+// perturb and estimate kernels each regenerate the noise instead of reading
+// an N x n array: the pass moves 4n + 8Nn bytes (antithetic) instead of
+// about 4n + 20Nn.  The normals come from Philox-4x64-10 (Salmon et al.,
+// SC 2011) blocks at counter (block, i, 0, 0) under key (seed, 0), through
+// the Box-Muller transform.  Block 64 s + l (segment s of 512 parameters,
+// slot l < 64) covers parameters 512 s + 4 l + e (words 0 and 1) and
+// 512 s + 256 + 4 l + e (words 2 and 3), e < 4; even e takes its word's cosine
+// normal, odd e the sine one.  A lane owns one block, so the 64 lanes of a
+// wave own one segment and each of the wave's two 128-bit store
+// instructions writes one contiguous 1 KiB run.
+
+constexpr uint64_t kPhiloxM0 = 0xD2E7470EE14C6C93ull;
+constexpr uint64_t kPhiloxM1 = 0xCA5A826395121157ull;
+constexpr uint64_t kPhiloxW0 = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kPhiloxW1 = 0xBB67AE8584CAA73Bull;
+
+// Ten rounds of Philox-4x64: per round the two 64 x 64 -> 128-bit products
+// M0 c0 and M1 c2, then c <- (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0); the
+// key advances by the Weyl increments between rounds.  The counter here is
+// (block, sample, 0, 0) and the key (seed, 0).
+__device__ __forceinline__ void philox_block(uint64_t block, uint64_t sample, uint64_t seed, uint64_t out[4]) {
+  uint64_t c0 = block, c1 = sample, c2 = 0, c3 = 0;
+  uint64_t k0 = seed, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += kPhiloxW0;
+      k1 += kPhiloxW1;
+    }
+    const uint64_t lo0 = kPhiloxM0 * c0, hi0 = __umul64hi(kPhiloxM0, c0);
+    const uint64_t lo1 = kPhiloxM1 * c2, hi1 = __umul64hi(kPhiloxM1, c2);
+    const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  out[0] = c0;
+  out[1] = c1;
+  out[2] = c2;
+  out[3] = c3;
+}
+
+// Box-Muller on one 64-bit word: 24-bit uniforms u1 = (lo/2^8 + 1) 2^-24 in
+// (0, 1] and u2 = (hi/2^8) 2^-24 in [0, 1), exact in fp32; r = sqrt(-2 ln u1),
+// za = r cos(2 pi u2), zb = r sin(2 pi u2).  logf, sqrtf and sincospif are
+// accurate to a few ulp, so each normal is within a few fp32 ulp of r of its
+// exact value.
+__device__ __forceinline__ void box_muller(uint64_t w, float& za, float& zb) {
+  const uint32_t lo = static_cast<uint32_t>(w), hi = static_cast<uint32_t>(w >> 32);
+  const float u1 = static_cast<float>((lo >> 8) + 1u) * 0x1p-24f;
+  const float u2 = static_cast<float>(hi >> 8) * 0x1p-24f;
+  const float r = sqrtf(-2.0f * logf(u1));
+  float sn, cs;
+  sincospif(2.0f * u2, &sn, &cs);
+  za = r * cs;
+  zb = r * sn;
+}
+
+// The eight normals of block `block` of sample `sample`: z[0..3] belong to
+// the block's first four parameters, z[4..7] to its second four.
+__device__ __forceinline__ void noise8(uint64_t block, uint64_t sample, uint64_t seed, float z[8]) {
+  uint64_t w[4];
+  philox_block(block, sample, seed, w);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) box_muller(w[q], z[2 * q], z[2 * q + 1]);
+}
+
+// First parameter of the two runs of four that block b covers.
+__device__ __forceinline__ int64_t run_start(int64_t b, int h) { return 512 * (b >> 6) + 256 * h + 4 * (b & 63); }
+
+// Weight of sample i from the caller's evaluations f (method 0 plain: f_i;
+// 1 baseline: f_i - f0; 2 antithetic: f_i - f_{N+i}).
+__device__ __forceinline__ float es_weight(const float* __restrict__ f, const float* __restrict__ f0, int64_t N,
+                                           int method, int64_t i) {
+  if (method == 0) return f[i];
+  if (method == 1) return f[i] - *f0;
+  return f[i] - f[N + i];
+}
+
+constexpr int kGRows = 8;  // samples per lane in the Gaussian perturb
+
+// Grid: x over Philox blocks (one per lane), y over groups of kGRows samples.
+// A lane reads its eight theta values once and writes its eight parameters
+// of every sample of the group (and of the antithetic rows).  VEC: n % 4 == 0
+// and 16-byte aligned theta and out, so each run of four moves as one
+// 128-bit access.
+template <bool VEC>
+__global__ __launch_bounds__(kEB) void es_perturb_gauss(const float* theta, int64_t N, int64_t n, uint64_t seed,
+                                                         float sigma, int antithetic, float* out) {
+  const int64_t b = (int64_t)blockIdx.x * kEB + threadIdx.x;
+  const int64_t j[2] = {run_start(b, 0), run_start(b, 1)};
+  if (j[0] >= n) return;
+  int cnt[2];
+  float t[8];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int64_t left = n - j[h];
+    cnt[h] = left <= 0 ? 0 : (left < 4 ? (int)left : 4);
+    if (VEC) {
+      const f32x4 a = cnt[h] ? *reinterpret_cast<const f32x4*>(theta + j[h]) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) t[4 * h + e] = a[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) t[4 * h + e] = e < cnt[h] ? theta[j[h] + e] : 0.0f;
+    }
+  }
+  const int64_t i0 = (int64_t)blockIdx.y * kGRows;
+  const int64_t i1 = i0 + kGRows < N ? i0 + kGRows : N;
+  for (int64_t i = i0; i < i1; ++i) {
+    float z[8], a[8], m[8];
+    noise8(b, i, seed, z);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      a[e] = fmaf(sigma, z[e], t[e]);
+      m[e] = fmaf(-sigma, z[e], t[e]);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (!cnt[h]) continue;
+      float* row = out + i * n + j[h];
+      float* rowm = out + (N + i) * n + j[h];
+      if (VEC) {
+        st(reinterpret_cast<f32x4*>(row), f32x4{a[4 * h], a[4 * h + 1], a[4 * h + 2], a[4 * h + 3]});
+        if (antithetic) st(reinterpret_cast<f32x4*>(rowm), f32x4{m[4 * h], m[4 * h + 1], m[4 * h + 2], m[4 * h + 3]});
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (e < cnt[h]) {
+            row[e] = a[4 * h + e];
+            if (antithetic) rowm[e] = m[4 * h + e];
+          }
+      }
+    }
+  }
+}
+
+// Each lane owns the eight gradient entries of one Philox block and walks
+// the N samples in order, regenerating the block's noise and accumulating
+// w_i z_ij in fp32; the result is scaled once at the end.
+template <bool VEC>
+__global__ __launch_bounds__(kEB) void es_estimate_gauss(const float* __restrict__ f, const float* __restrict__ f0,
+                                                          int64_t N, int method, int64_t n, uint64_t seed, float scale,
+                                                          float* grad) {
+  const int64_t b = (int64_t)blockIdx.x * kEB + threadIdx.x;
+  const int64_t j[2] = {run_start(b, 0), run_start(b, 1)};
+  if (j[0] >= n) return;
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+  for (int64_t i = 0; i < N; ++i) {
+    const float wi = es_weight(f, f0, N, method, i);
+    float z[8];
+    noise8(b, i, seed, z);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = fmaf(wi, z[e], acc[e]);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int64_t left = n - j[h];
+    if (left <= 0) continue;
+    float* g = grad + j[h];
+    if (VEC) {
+      st(reinterpret_cast<f32x4*>(g),
+         f32x4{scale * acc[4 * h], scale * acc[4 * h + 1], scale * acc[4 * h + 2], scale * acc[4 * h + 3]});
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e < left) g[e] = scale * acc[4 * h + e];
+    }
+  }
+}
+
+// weights_i = scale * (method difference of the evaluations), for the
+// explicit-noise estimate.
+__global__ __launch_bounds__(kEB) void es_weights_kernel(const float* __restrict__ f, const float* __restrict__ f0,
+                                                          int64_t N, int method, float scale, float* w) {
+  const int64_t i = (int64_t)blockIdx.x * kEB + threadIdx.x;
+  if (i < N) w[i] = scale * es_weight(f, f0, N, method, i);
+}
+
 bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool al4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
@@ -257,5 +442,88 @@ extern "C" int diffopt_es_estimate(const float* noise, const float* weights, int
     hipLaunchKernelGGL(es_estimate_scalar, dim3((unsigned)bx), dim3(kEB), 0, st, noise, weights, num_samples, n,
                        (float)scale, grad);
   }
+  return launch_status(who);
+}
+
+namespace {
+
+bool es_method_ok(int32_t method) { return method >= 0 && method <= 2; }
+
+// 1 / (N s), or 1 / (2 N s) for antithetic sampling, formed in fp64 and
+// rounded once.
+float es_scale(int32_t method, int64_t num_samples, double sigma) {
+  return static_cast<float>(1.0 / ((method == 2 ? 2.0 : 1.0) * static_cast<double>(num_samples) * sigma));
+}
+
+}  // namespace
+
+extern "C" int diffopt_es_perturb_gaussian(const float* params, int64_t n, int64_t num_samples, uint64_t seed,
+                                           double sigma, int32_t antithetic, float* out, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_es_perturb_gaussian";
+  if (n < 0 || num_samples < 0) return fail(DIFFOPT_EINVAL, "%s: n and num_samples must be >= 0", who);
+  if (!std::isfinite(sigma)) return fail(DIFFOPT_EINVAL, "%s: sigma must be finite", who);
+  if (n == 0 || num_samples == 0) return DIFFOPT_OK;
+  if (!params || !out) return fail(DIFFOPT_EINVAL, "%s: null required pointer", who);
+  if (!al4(params) || !al4(out)) return fail(DIFFOPT_EINVAL, "%s: pointers must be 4-byte aligned", who);
+  const int64_t gy = (num_samples + kGRows - 1) / kGRows;
+  if (gy > 65535) return fail(DIFFOPT_EINVAL, "%s: num_samples too large (max %d)", who, 65535 * kGRows);
+  const int64_t blocks = 64 * ((n + 511) / 512);  // Philox blocks: 64 per 512 parameters
+  const int64_t bx = (blocks + kEB - 1) / kEB;
+  if (bx > 0x7fffffff) return fail(DIFFOPT_EINVAL, "%s: n too large", who);
+  hipStream_t st = as_stream(stream);
+  const dim3 grid((unsigned)bx, (unsigned)gy);
+  if (n % 4 == 0 && al16(params) && al16(out))
+    hipLaunchKernelGGL(es_perturb_gauss<true>, grid, dim3(kEB), 0, st, params, num_samples, n, seed, (float)sigma,
+                       antithetic ? 1 : 0, out);
+  else
+    hipLaunchKernelGGL(es_perturb_gauss<false>, grid, dim3(kEB), 0, st, params, num_samples, n, seed, (float)sigma,
+                       antithetic ? 1 : 0, out);
+  return launch_status(who);
+}
+
+extern "C" int diffopt_es_estimate_gaussian(const float* fvals, const float* f0, int64_t num_samples, int32_t method,
+                                            int64_t n, uint64_t seed, double sigma, float* grad, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_es_estimate_gaussian";
+  if (n < 0 || num_samples < 0) return fail(DIFFOPT_EINVAL, "%s: n and num_samples must be >= 0", who);
+  if (!es_method_ok(method)) return fail(DIFFOPT_EINVAL, "%s: method must be 0 (plain), 1 (baseline) or 2 "
+                                         "(antithetic)", who);
+  if (!std::isfinite(sigma) || sigma == 0.0) return fail(DIFFOPT_EINVAL, "%s: sigma must be finite and nonzero", who);
+  if (n == 0) return DIFFOPT_OK;
+  if (!grad || (num_samples > 0 && (!fvals || (method == 1 && !f0))))
+    return fail(DIFFOPT_EINVAL, "%s: null required pointer (f0 is required by the baseline method)", who);
+  if (!al4(grad) || (num_samples > 0 && !al4(fvals))) return fail(DIFFOPT_EINVAL, "%s: pointers must be 4-byte "
+                                                                  "aligned", who);
+  const int64_t blocks = 64 * ((n + 511) / 512);  // Philox blocks: 64 per 512 parameters
+  const int64_t bx = (blocks + kEB - 1) / kEB;
+  if (bx > 0x7fffffff) return fail(DIFFOPT_EINVAL, "%s: n too large", who);
+  const float scale = num_samples > 0 ? es_scale(method, num_samples, sigma) : 0.0f;
+  hipStream_t st = as_stream(stream);
+  if (n % 4 == 0 && al16(grad))
+    hipLaunchKernelGGL(es_estimate_gauss<true>, dim3((unsigned)bx), dim3(kEB), 0, st, fvals, f0, num_samples,
+                       (int)method, n, seed, scale, grad);
+  else
+    hipLaunchKernelGGL(es_estimate_gauss<false>, dim3((unsigned)bx), dim3(kEB), 0, st, fvals, f0, num_samples,
+                       (int)method, n, seed, scale, grad);
+  return launch_status(who);
+}
+
+extern "C" int diffopt_es_weights(const float* fvals, const float* f0, int64_t num_samples, int32_t method,
+                                  double sigma, float* weights, void* stream) {
+  clear_error();
+  static const char* who = "diffopt_es_weights";
+  if (num_samples < 0) return fail(DIFFOPT_EINVAL, "%s: num_samples must be >= 0", who);
+  if (!es_method_ok(method)) return fail(DIFFOPT_EINVAL, "%s: method must be 0 (plain), 1 (baseline) or 2 "
+                                         "(antithetic)", who);
+  if (!std::isfinite(sigma) || sigma == 0.0) return fail(DIFFOPT_EINVAL, "%s: sigma must be finite and nonzero", who);
+  if (num_samples == 0) return DIFFOPT_OK;
+  if (!fvals || !weights || (method == 1 && !f0))
+    return fail(DIFFOPT_EINVAL, "%s: null required pointer (f0 is required by the baseline method)", who);
+  if (!al4(fvals) || !al4(weights)) return fail(DIFFOPT_EINVAL, "%s: pointers must be 4-byte aligned", who);
+  const int64_t bx = (num_samples + kEB - 1) / kEB;
+  if (bx > 0x7fffffff) return fail(DIFFOPT_EINVAL, "%s: num_samples too large", who);
+  hipLaunchKernelGGL(es_weights_kernel, dim3((unsigned)bx), dim3(kEB), 0, as_stream(stream), fvals, f0, num_samples,
+                     (int)method, es_scale(method, num_samples, sigma), weights);
   return launch_status(who);
 }

@@ -67,6 +67,9 @@ def _load_library():
                                                     vp]),
         "diffopt_es_perturb": (ctypes.c_int, [vp, vp, i64, i64, f64, i32, vp, vp]),
         "diffopt_es_estimate": (ctypes.c_int, [vp, vp, i64, i64, f64, vp, vp]),
+        "diffopt_es_perturb_gaussian": (ctypes.c_int, [vp, i64, i64, ctypes.c_uint64, f64, i32, vp, vp]),
+        "diffopt_es_estimate_gaussian": (ctypes.c_int, [vp, vp, i64, i32, i64, ctypes.c_uint64, f64, vp, vp]),
+        "diffopt_es_weights": (ctypes.c_int, [vp, vp, i64, i32, f64, vp, vp]),
     }
     for name, (res, args) in sig.items():
         if not hasattr(lib, name):
@@ -498,3 +501,46 @@ def es_estimate(noise, weights, scale, grad, stream=None) -> None:
         raise ValueError("noise must be [N, n] with N = weights.numel(), n = grad.numel()")
     _check(_lib.diffopt_es_estimate(_addr(noise, "noise"), _addr(weights, "weights"), int(N), int(n), float(scale),
                                     _addr(grad, "grad"), _stream(stream)))
+
+
+ES_METHODS = {"plain": 0, "baseline": 1, "antithetic": 2}
+
+
+def _es_method(method) -> int:
+    if method not in ES_METHODS:
+        raise ValueError("method must be one of %s" % sorted(ES_METHODS))
+    return ES_METHODS[method]
+
+
+def es_perturb_gaussian(params, num_samples: int, seed: int, sigma, antithetic, out, stream=None) -> None:
+    """diffopt_es_perturb_gaussian: out is [N, n] (or [2N, n] if antithetic); the noise is generated in the kernel."""
+    n = params.numel()
+    if out.numel() != (2 if antithetic else 1) * num_samples * n:
+        raise ValueError("out must be [N or 2N, n]")
+    _check(_lib.diffopt_es_perturb_gaussian(_addr(params, "params"), int(n), int(num_samples),
+                                            int(seed) & ((1 << 64) - 1), float(sigma), int(bool(antithetic)),
+                                            _addr(out, "out"), _stream(stream)))
+
+
+def es_estimate_gaussian(fvals, method: str, num_samples: int, seed: int, sigma, grad, f0=None, stream=None) -> None:
+    """diffopt_es_estimate_gaussian: fvals [N] (plain, baseline) or [2N] (antithetic), f0 a device scalar
+    (baseline); the weights, the scale and the noise are formed in the kernel."""
+    m = _es_method(method)
+    if fvals.numel() != (2 if m == 2 else 1) * num_samples:
+        raise ValueError("fvals must hold %s evaluations" % ("2N" if m == 2 else "N"))
+    if m == 1 and f0 is None:
+        raise ValueError("the baseline method needs f0 = f(theta)")
+    _check(_lib.diffopt_es_estimate_gaussian(_addr(fvals, "fvals"), _addr(f0, "f0", n=1) if m == 1 else None,
+                                             int(num_samples), m, int(grad.numel()), int(seed) & ((1 << 64) - 1),
+                                             float(sigma), _addr(grad, "grad"), _stream(stream)))
+
+
+def es_weights(fvals, method: str, num_samples: int, sigma, weights, f0=None, stream=None) -> None:
+    """diffopt_es_weights: weights [N] = scale * w for diffopt_es_estimate with scale 1."""
+    m = _es_method(method)
+    if fvals.numel() != (2 if m == 2 else 1) * num_samples or weights.numel() != num_samples:
+        raise ValueError("fvals must hold N (2N antithetic) evaluations and weights N entries")
+    if m == 1 and f0 is None:
+        raise ValueError("the baseline method needs f0 = f(theta)")
+    _check(_lib.diffopt_es_weights(_addr(fvals, "fvals"), _addr(f0, "f0", n=1) if m == 1 else None,
+                                   int(num_samples), m, float(sigma), _addr(weights, "weights"), _stream(stream)))

@@ -178,6 +178,9 @@ def test_leaf_direct_and_batched_entry_points_in_hip_graph_replay():
     theta, noise = torch.randn(4096, device="cuda", generator=gen), torch.randn(8, 4096, device="cuda", generator=gen)
     wts = torch.randn(8, device="cuda", generator=gen)
     pts, eg = torch.empty(16, 4096, device="cuda"), torch.empty(4096, device="cuda")
+    fv = torch.randn(16, device="cuda", generator=gen)
+    gtheta = torch.randn(4100, device="cuda", generator=gen)  # n % 8 == 4: a half block at the end
+    gpts, geg, gw = torch.empty(16, 4100, device="cuda"), torch.empty(4100, device="cuda"), torch.empty(8, device="cuda")
 
     def run():
         P.tree_flatten_batch(table, [P_["p"]] + [P_["g%d" % k] for k in range(K)], flats)
@@ -196,10 +199,13 @@ def test_leaf_direct_and_batched_entry_points_in_hip_graph_replay():
                            P_["rdg"], P_["rdv"])
         P.es_perturb(theta, noise, 0.1, True, pts)
         P.es_estimate(noise, wts, 0.5, eg)
+        P.es_perturb_gaussian(gtheta, 8, 77, 0.1, True, gpts)
+        P.es_estimate_gaussian(fv, "antithetic", 8, 77, 0.1, geg)
+        P.es_weights(fv, "antithetic", 8, 0.1, gw)
 
     run()
     torch.cuda.synchronize()
-    outs = [x for leaves in out.values() for x in leaves] + flats + [pts, eg]
+    outs = [x for leaves in out.values() for x in leaves] + flats + [pts, eg, gpts, geg, gw]
     eager = [x.clone() for x in outs]
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())

@@ -181,25 +181,33 @@ def test_flat_sgd_rmsprop_step(which):
         assert_mag_close(got, r, m, BWD_RTOL, "bwd output %d" % i)
 
 
-def test_es_step():
+@pytest.mark.parametrize("noise_input", [False, True])
+def test_es_step(noise_input):
     # ResNet-18 size, 64 antithetic rows: sampled columns of the points and
-    # of the estimate (every column is computed from its own column of noise)
+    # of the estimate (every column is computed from its own column of noise:
+    # regenerated by the oracle from the seed, or read from the noise array)
     import paper_2211_06934_amd as P
     b = _bench()
-    S = b.setup_es(torch, P, WORKLOADS["resnet18_k1"]())
+    S = b.setup_es(torch, P, WORKLOADS["resnet18_k1"](), noise_input)
     b.step_es(P, S)
     torch.cuda.synchronize()
     idx = _sample(S["n"], 50_000, 15)
     cols = lambda t: t.index_select(1, idx).cpu().numpy().astype(np.float64)  # noqa: E731
     theta = S["theta"].index_select(0, idx).cpu().numpy().astype(np.float64)
-    Z = cols(S["noise"])
     sigma, N = S["sigma"], S["N"]
-    mag = np.abs(theta)[None, :] + sigma * np.abs(np.concatenate([Z, Z]))
+    if noise_input:
+        Z = cols(S["noise"])
+        R = np.abs(Z)
+    else:
+        Z, R = oracle.es_gaussian_noise_cols(N, idx.cpu().numpy(), S["seed"])
+    mag = np.abs(theta)[None, :] + sigma * np.concatenate([R, R])
     assert_mag_close(cols(S["pts"]), oracle.es_perturb(theta, Z, sigma, True), mag, FWD_RTOL, "perturb")
-    w = S["w"].cpu().numpy().astype(np.float64)
-    scale = 1.0 / (2 * N * sigma)
+    f = S["fvals"].cpu().numpy().astype(np.float64)
+    w, scale = oracle.es_weights(f, "antithetic", sigma)
+    terms = oracle.es_weight_terms(f, "antithetic")
     g = S["grad"].index_select(0, idx).cpu().numpy().astype(np.float64)
-    assert_mag_close(g, oracle.es_estimate(Z, w, scale), oracle.es_estimate_mag(Z, w, scale), BWD_RTOL, "estimate")
+    assert_mag_close(g, oracle.es_estimate(Z, w, scale), oracle.es_estimate_mag(R, terms, scale), BWD_RTOL,
+                     "estimate")
 
 
 def test_stepwise_pass():
@@ -230,3 +238,32 @@ def test_stepwise_pass():
     pairs = [(pK, S["pK"]), (mt[K], S["mu"][K]), (vt[K], S["nu"][K]), (dm0, S["dm0"]), (dv0, S["dv0"])]
     for a, c in pairs + list(zip(dg, S["dg"])):
         assert torch.equal(a.view(torch.int32), c.view(torch.int32))
+
+
+@pytest.mark.parametrize("name", ["tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10"])
+def test_small_tree_forms_agree_bit_for_bit(name):
+    # the three forms the small-trees benchmark times -- pack + fused K-step +
+    # unpack, leaf-direct fused K-step, leaf-direct one launch per step --
+    # compute every element with the same operations, so p_K, every dg_k and
+    # the initial-state cotangents agree bit for bit
+    import paper_2211_06934_amd as P
+    b = _bench()
+    w = WORKLOADS[name]()
+    A = b.setup_tree(torch, P, w, "recompute")
+    b.step_tree(P, A)
+    K, n = A["K"], A["n"]
+    ref = [A["pK"]] + A["dg"] + [A["dm0"], A["dv0"]]
+    for stepwise in (False, True):
+        S = b.setup_treemap(torch, P, w, "stored" if stepwise else "recompute", stepwise=stepwise)
+        (b.step_treemap_stepwise if stepwise else b.step_treemap)(P, S)
+
+        def flat(ptrs):
+            out = torch.empty(n, device="cuda")
+            P.tree_flatten(S["table"], ptrs, out)
+            return out
+
+        got = [flat(S["pK"])] + [flat(d) for d in S["dg"]] + [flat(S["dm0"]), flat(S["dv0"])]
+        torch.cuda.synchronize()
+        for i, (x, y) in enumerate(zip(got, ref)):
+            assert torch.equal(x.view(torch.int32), y.view(torch.int32)), (name, stepwise, i)
+    assert K == len(A["dg"])

@@ -90,9 +90,168 @@ def test_zero_order_fn_autograd():
         return ((x - c) ** 2).sum(-1)
 
     theta = torch.zeros(n, device="cuda", requires_grad=True)
-    gen = torch.Generator(device="cuda").manual_seed(0)
-    y = P.autograd.ZeroOrderFn.apply(theta, fn, 0.05, 4096, "antithetic", gen)
+    y = P.autograd.ZeroOrderFn.apply(theta, fn, 0.05, 4096, "antithetic", 0)
     (gt,) = torch.autograd.grad(2.0 * y, theta)
     exact = 2.0 * 2.0 * (theta.detach() - c)
     rel = (torch.linalg.norm(gt - exact) / torch.linalg.norm(exact)).item()
     assert np.isfinite(rel) and rel < 0.2, rel
+
+
+# ---------------------------------------------------------------- in-kernel noise
+# The noise is a function of (seed, sample, parameter) defined in the header;
+# the oracle generates it from the same definition in fp64.  Each computed
+# normal z = r cos(a) (or r sin(a)) is judged against its radius r: the
+# transform's fp32 error is a few ulp of r, so the bar is 1e-6 r.
+
+NOISE_RTOL = 1e-6
+
+
+def _mag_fwd(theta, r, sigma, antithetic):
+    return np.abs(theta)[None, :] + abs(sigma) * (np.concatenate([r, r]) if antithetic else r)
+
+
+@pytest.mark.parametrize("n", [1, 3, 4, 7, 8, 9, 12, 4099, (1 << 20) + 4])
+@pytest.mark.parametrize("N", [1, 5, 8, 17])
+def test_gaussian_noise_matches_oracle(n, N):
+    import paper_2211_06934_amd as P
+    seed = 0x5EED0000 + 31 * n + N
+    out = torch.empty(2 * N, n, device="cuda")
+    P.es_perturb_gaussian(torch.zeros(n, device="cuda"), N, seed, 1.0, True, out)
+    torch.cuda.synchronize()
+    z = oracle.es_gaussian_noise(N, n, seed)
+    r = oracle.es_gaussian_noise_radius(N, n, seed)
+    got = out.cpu().numpy().astype(np.float64)
+    assert_mag_close(got[:N], z, r, NOISE_RTOL, "noise")
+    assert np.array_equal(got[N:], -got[:N])  # the antithetic rows are exact negations at theta = 0
+    # the noise is a function of (seed, sample, parameter) only: a prefix of
+    # the parameters and of the samples gives the same values, bit for bit
+    if n > 8 and N > 1:
+        part = torch.empty(N - 1, n - 5, device="cuda")
+        P.es_perturb_gaussian(torch.zeros(n - 5, device="cuda"), N - 1, seed, 1.0, False, part)
+        torch.cuda.synchronize()
+        assert np.array_equal(part.cpu().numpy(), out[:N - 1, :n - 5].cpu().numpy())
+
+
+@pytest.mark.parametrize("n", [3, 4099, 1 << 16])
+@pytest.mark.parametrize("antithetic", [False, True])
+def test_gaussian_perturb_matches_oracle(n, antithetic):
+    import paper_2211_06934_amd as P
+    N, sigma, seed = 11, 0.05, 12345
+    theta = normal(n, 0.05, "ges", "p0", n % 89)
+    out = torch.empty((2 if antithetic else 1) * N, n, device="cuda")
+    P.es_perturb_gaussian(_dev(theta), N, seed, sigma, antithetic, out)
+    torch.cuda.synchronize()
+    z = oracle.es_gaussian_noise(N, n, seed)
+    ref = oracle.es_perturb(theta, z, sigma, antithetic)
+    mag = _mag_fwd(theta, oracle.es_gaussian_noise_radius(N, n, seed), sigma, antithetic)
+    assert_mag_close(out.cpu().numpy(), ref, mag, FWD_RTOL, "perturb")
+
+
+@pytest.mark.parametrize("n", [1, 5, 8, 4099, (1 << 18) + 4])
+@pytest.mark.parametrize("method", ["plain", "baseline", "antithetic"])
+def test_gaussian_estimate_matches_oracle(n, method):
+    import paper_2211_06934_amd as P
+    N, sigma, seed = 13, 0.05, 2024 + n
+    f = normal((2 if method == "antithetic" else 1) * N, 1.0, "ges", "cot_m", N) + 3.0
+    f0 = np.float32(2.5)
+    g = torch.empty(n, device="cuda")
+    P.es_estimate_gaussian(_dev(f), method, N, seed, sigma, g, f0=_dev(np.array([f0])))
+    torch.cuda.synchronize()
+    z = oracle.es_gaussian_noise(N, n, seed)
+    w, scale = oracle.es_weights(f, method, sigma, f0=float(f0))
+    terms = oracle.es_weight_terms(f, method, f0=float(f0))
+    mag = oracle.es_estimate_mag(oracle.es_gaussian_noise_radius(N, n, seed), terms, scale)
+    assert_mag_close(g.cpu().numpy(), oracle.es_estimate(z, w, scale), mag, BWD_RTOL, "estimate " + method)
+
+
+def test_gaussian_paths_misaligned_and_empty():
+    import paper_2211_06934_amd as P
+    n, N, seed = 4096, 6, 99
+    buf = torch.zeros(n + 1, device="cuda")
+    theta = buf[1:]  # 4-byte but not 16-byte aligned: the element path
+    theta.copy_(_dev(normal(n, 0.05, "ges", "p0", 3)))
+    out = torch.empty(N * n + 1, device="cuda")[1:].view(N, n)
+    P.es_perturb_gaussian(theta, N, seed, 0.1, False, out)
+    ref = torch.empty(N, n, device="cuda")
+    P.es_perturb_gaussian(theta.clone(), N, seed, 0.1, False, ref)
+    f = _dev(normal(N, 1.0, "ges", "cot_v", 3))
+    g1 = torch.empty(n + 1, device="cuda")[1:]
+    g2 = torch.empty(n, device="cuda")
+    P.es_estimate_gaussian(f, "plain", N, seed, 0.1, g1)
+    P.es_estimate_gaussian(f, "plain", N, seed, 0.1, g2)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref) and torch.equal(g1, g2)  # vector and element paths agree bit for bit
+    # no samples: the estimate is zero; no parameters: nothing is touched
+    z = torch.full((n,), 7.0, device="cuda")
+    P.es_estimate_gaussian(torch.empty(0, device="cuda"), "plain", 0, seed, 0.1, z)
+    P.es_perturb_gaussian(torch.empty(0, device="cuda"), 4, seed, 0.1, True, torch.empty(0, device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.all(z == 0)
+    with pytest.raises(P.DiffoptError):
+        P.es_estimate_gaussian(f, "plain", N, seed, 0.0, g2)  # sigma = 0
+    with pytest.raises(ValueError):
+        P.es_estimate_gaussian(f, "baseline", N, seed, 0.1, g2)  # f0 missing
+
+
+@pytest.mark.parametrize("method", ["plain", "baseline", "antithetic"])
+def test_es_weights_match_oracle(method):
+    import paper_2211_06934_amd as P
+    N, sigma = 37, 0.02
+    f = normal((2 if method == "antithetic" else 1) * N, 1.0, "ges", "cot_p", 17) + 1.0
+    f0 = np.float32(-0.75)
+    w = torch.empty(N, device="cuda")
+    P.es_weights(_dev(f), method, N, sigma, w, f0=_dev(np.array([f0])))
+    torch.cuda.synchronize()
+    wr, scale = oracle.es_weights(f, method, sigma, f0=float(f0))
+    assert_mag_close(w.cpu().numpy(), wr * scale, oracle.es_weight_terms(f, method, f0=float(f0)) * abs(scale),
+                     FWD_RTOL, "weights " + method)
+
+
+def test_es_gradient_gaussian_recovers_quadratic_gradient():
+    # the default path: in-kernel noise, weights formed in the kernel; with
+    # many antithetic samples the estimate of a quadratic's gradient converges
+    import paper_2211_06934_amd as P
+    n, N = 48, 8192
+    rng = np.random.default_rng(4)
+    A = rng.normal(size=(n, n)).astype(np.float32)
+    A = torch.tensor(A @ A.T / n, device="cuda")
+    b = torch.tensor(rng.normal(size=n).astype(np.float32), device="cuda")
+    theta = torch.tensor(rng.normal(size=n).astype(np.float32), device="cuda")
+
+    def fn(x):
+        return 0.5 * ((x @ A) * x).sum(-1) + x @ b
+
+    exact = A @ theta + b
+    for method in ("antithetic", "baseline"):
+        g = P.es_gradient(fn, theta, 0.05, N, method, seed=7)
+        rel = (torch.linalg.norm(g - exact) / torch.linalg.norm(exact)).item()
+        assert rel < 8 * np.sqrt(n / N) * (1 if method == "antithetic" else 4), (method, rel)
+    # the same seed gives the same estimate, bit for bit
+    assert torch.equal(P.es_gradient(fn, theta, 0.05, 64, "antithetic", seed=3),
+                       P.es_gradient(fn, theta, 0.05, 64, "antithetic", seed=3))
+
+
+def test_es_gradient_with_a_caller_sampler_matches_oracle():
+    # Listing 3's customisable sampler: the noise comes from the caller, the
+    # points and the estimate from the explicit-noise kernels, the weights
+    # from diffopt_es_weights
+    import paper_2211_06934_amd as P
+    n, N, sigma = 1000, 9, 0.1
+    Z = normal(N * n, 1.0, "ges", "misc", 41).reshape(N, n) * 0.5  # a narrower distribution
+    theta = _dev(normal(n, 1.0, "ges", "p0", 41))
+    c = _dev(normal(n, 1.0, "ges", "grad", 41))
+
+    def fn(x):
+        return (x * c).sum(-1) + 0.25 * (x * x).sum(-1)
+
+    for method in ("plain", "baseline", "antithetic"):
+        g = P.es_gradient(fn, theta, sigma, N, method, sample=lambda N_, n_: _dev(Z))
+        pts = oracle.es_perturb(theta.cpu().numpy(), Z, sigma, method == "antithetic")
+        fv = (pts * c.cpu().numpy()).sum(-1) + 0.25 * (pts * pts).sum(-1)
+        f0 = float(fn(theta.reshape(1, -1)).item())
+        w, scale = oracle.es_weights(fv, method, sigma, f0=f0)
+        ref = oracle.es_estimate(Z, w, scale)
+        # the caller's f runs in fp32 on the GPU: judge against its values'
+        # rounding (1e-6 relative) carried through the weights
+        mag = oracle.es_estimate_mag(Z, oracle.es_weight_terms(fv, method, f0=f0), scale)
+        assert_mag_close(g.cpu().numpy(), ref, mag, 1e-5 * 100, method)

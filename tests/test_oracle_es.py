@@ -176,3 +176,23 @@ def test_weights_recover_linear_and_quadratic_gradients_exactly():
     assert np.allclose(oracle.es_weights(fv, "baseline", 0.1, f0=2.0)[0], fv - 2.0, rtol=0, atol=0)
     assert oracle.es_weights(fv, "plain", 0.1)[1] == 1.0 / (N * 0.1)
     assert oracle.es_weights(np.concatenate([fv, fv]), "antithetic", 0.1)[1] == 1.0 / (2 * N * 0.1)
+
+
+def test_noise_radius_is_the_pair_radius():
+    # r^2 = za^2 + zb^2 for the two normals of one word, and |z| <= r
+    N, n = 5, 64
+    z = oracle.es_gaussian_noise(N, n, 77)
+    r = oracle.es_gaussian_noise_radius(N, n, 77)
+    assert np.allclose(r[:, 0::2] ** 2, z[:, 0::2] ** 2 + z[:, 1::2] ** 2, rtol=1e-13, atol=0)
+    assert np.array_equal(r[:, 0::2], r[:, 1::2])
+    assert np.all(np.abs(z) <= r * (1 + 1e-15))
+    assert np.array_equal(oracle.es_gaussian_noise_radius(N, 13, 77), r[:, :13])
+
+
+def test_noise_at_chosen_columns_is_the_same_noise():
+    N, n, seed = 3, 77, 2**63 + 5
+    z = oracle.es_gaussian_noise(N, n, seed)
+    r = oracle.es_gaussian_noise_radius(N, n, seed)
+    cols = [76, 0, 9, 8, 7, 40, 9]
+    zc, rc = oracle.es_gaussian_noise_cols(N, cols, seed)
+    assert np.array_equal(zc, z[:, cols]) and np.array_equal(rc, r[:, cols])
