@@ -1059,7 +1059,7 @@ def main():
         w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
                        "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
                        "es_resnet18": "resnet18_k1", "es_resnet18_noise": "resnet18_k1", "flat_1b_zero_mv": "flat_1b",
-                       "many_small_stepwise": "many_small"}.get(a.workload, a.workload)]()
+                       "many_small_stepwise": "many_small", "small_trees": "tiny_mlp"}.get(a.workload, a.workload)]()
     if a.workload == "small_trees":
         table = small_trees(torch, P, max(a.steps, 100), max(a.warmup, 5))
         t = table["tiny_mlp"]["leaf_direct_fused"]

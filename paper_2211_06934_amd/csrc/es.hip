@@ -257,7 +257,10 @@ __device__ __forceinline__ float es_weight(const float* __restrict__ f, const fl
   return f[i] - f[N + i];
 }
 
-constexpr int kGRows = 8;  // samples per lane in the Gaussian perturb
+#ifndef DIFFOPT_ES_GROWS
+#define DIFFOPT_ES_GROWS 8
+#endif
+constexpr int kGRows = DIFFOPT_ES_GROWS;  // samples per lane in the Gaussian perturb
 
 // Grid: x over Philox blocks (one per lane), y over groups of kGRows samples.
 // A lane reads its eight theta values once and writes its eight parameters

@@ -7,8 +7,10 @@
 
 // Launch shape, chosen by measurement on MI355X (20,000 leaves, n ~ 1.2e8):
 // 256 threads x 2 groups per tile with streaming stores.  One group per lane
-// (any workgroup size) spends too long per staged window; 4 groups per lane,
-// and renumbering tiles so that each XCD walks a contiguous run, were slower.
+// (any workgroup size) spends too long per staged window; 4 groups per lane
+// (5-6% slower in a paired run on six allocations), 512-thread tiles (1-3%
+// slower), and renumbering tiles so that each XCD walks a contiguous eighth
+// of them, were slower.
 #ifndef DIFFOPT_TREE_U
 #define DIFFOPT_TREE_U 2  // groups (16-byte vectors) per lane per tile
 #endif

@@ -99,6 +99,31 @@ struct CopyBatch {
   uint64_t flat[kMaxBatch];              // flat buffers
 };
 
+// Tile order.  The dispatcher deals workgroups to the eight XCDs in turn, so
+// neighbouring tiles -- which share the source line that straddles their
+// boundary when source and destination are out of phase -- would run on
+// different XCDs and both fetch that line from HBM.  With DIFFOPT_TREE_RUN =
+// R > 1, each block of 8R workgroups takes 8R consecutive tiles so that the R
+// workgroups an XCD receives get R consecutive tiles (the chip still works
+// through one 8R-tile block at a time); a ragged last block keeps the plain
+// order.  Measured on the 20,000-leaf tree, four trees per launch: R = 4
+// fetches 1.019 of the algorithmic bytes against 1.042 for the plain order
+// (the rest is the table and the partial head/tail groups), at the same or
+// slightly better rate (pack 6.12 against 6.10 TB/s, unpack 6.24 against
+// 6.22, six paired allocations); R = 2 fell in between.
+#ifndef DIFFOPT_TREE_RUN
+#define DIFFOPT_TREE_RUN 4
+#endif
+
+__device__ __forceinline__ int64_t tree_tile(int64_t b, int64_t ntiles) {
+  constexpr int64_t R = DIFFOPT_TREE_RUN;
+  if (R <= 1) return b;
+  const int64_t base = b - b % (8 * R);
+  if (base + 8 * R > ntiles) return b;
+  const int64_t l = b - base;
+  return base + (l % 8) * R + l / 8;
+}
+
 template <int E, bool PACK>
 __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restrict__ seg,
                                                         const int64_t* __restrict__ tile_first, int64_t ngroups,
@@ -110,7 +135,7 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
   __shared__ int64_t s_bytes[kWindowMax];
   __shared__ uint64_t s_leaf[kWindowMax];
 
-  const int64_t b = blockIdx.x;
+  const int64_t b = tree_tile(blockIdx.x, gridDim.x);
   const int64_t j0 = tile_first[b];
   const int W = (int)(tile_first[b + 1] - j0 + 1);
   for (int t = threadIdx.x; t <= W; t += kTB) {
