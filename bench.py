@@ -32,6 +32,8 @@ Other workloads (--workload), each printing its own line:
   many_small_stepwise      the stepwise pass alone
   sgd_flat | rmsprop_flat | sgd_treemap | rmsprop_treemap
                            one fwd + bwd of the other fused optimizers
+  meta_loop                the fused step in a Listing-1 autograd loop (conv-net tree, host path
+                           included) beside the same loop on torch.optim's functional Adam
   small_trees              the small trees in three forms (pack + fused + unpack, leaf-direct
                            fused, leaf-direct one launch per step), HIP graph replay
   es_resnet18 [_noise]     ES perturb + estimate at the ResNet-18 size, noise generated in
@@ -132,7 +134,7 @@ def parse():
                     choices=["many_small", "flat_1b", "tiny_mlp", "convnet32", "resnet18_k1", "resnet18_k10",
                              "many_small_treemap", "sgd_flat", "rmsprop_flat", "sgd_treemap", "rmsprop_treemap",
                              "es_resnet18", "es_resnet18_noise", "adam_vs_torch", "flat_1b_zero_mv",
-                             "many_small_stepwise", "small_trees"])
+                             "many_small_stepwise", "small_trees", "meta_loop"])
     ap.add_argument("--trajectory", choices=["stored", "recompute"], default="recompute",
                     help="K-step driver: store every moment state for the backward, or store only the final one "
                          "(and every %d-th) and let the backward recompute the rest in registers" % REMAT_SPAN)
@@ -1020,6 +1022,67 @@ def small_trees(torch, P, steps, warmup):
     return table
 
 
+def meta_loop(torch, P, steps, warmup, K=5):
+    """The fused step in the loop a Listing-1 user writes, product path
+    included: K inner steps through AdamTreeFn (leaf-address arrays built per
+    call, outputs allocated per step, autograd recording), then the
+    meta-gradient by autograd through all of them, on the conv-net's 18
+    parameter tensors (112,261 parameters).  The inner gradient is that of the
+    quadratic L(p) = sum(c p^2) / 2, taken with create_graph, so the backward
+    carries Hessian-vector products between the fused VJPs as a model's would,
+    at negligible model cost.  Beside it, the same loop on torch.optim's
+    functional Adam in differentiable mode.  Returns microseconds per inner
+    step (forward and its share of the backward) for both."""
+    from torch.optim.adam import adam as torch_adam
+    from workloads import convnet_shapes
+    shapes = convnet_shapes()
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    p0 = [(torch.randn(s, device="cuda", generator=gen) * 0.05).requires_grad_() for s in shapes]
+    c = [torch.rand(s, device="cuda", generator=gen) for s in shapes]
+    table = P.tree.segment_table(shapes, torch.float32)
+    h = P.AdamHyper()
+
+    def fused():
+        ps = list(p0)
+        m = [torch.zeros_like(x) for x in ps]
+        v = [torch.zeros_like(x) for x in ps]
+        for k in range(K):
+            g = torch.autograd.grad(sum((ci * pi * pi).sum() for ci, pi in zip(c, ps)) * 0.5, ps, create_graph=True)
+            out = P.AdamTreeFn.apply(table, k, h, *ps, *g, *m, *v)
+            S = len(ps)
+            ps, m, v = list(out[:S]), list(out[S:2 * S]), list(out[2 * S:])
+        return torch.autograd.grad(sum(x.sum() for x in ps), p0)
+
+    def reference():
+        ps = [x.clone() for x in p0]
+        m = [torch.zeros_like(x) for x in ps]
+        v = [torch.zeros_like(x) for x in ps]
+        for k in range(K):
+            g = list(torch.autograd.grad(sum((ci * pi * pi).sum() for ci, pi in zip(c, ps)) * 0.5, ps,
+                                         create_graph=True))
+            ps, m, v = [x.clone() for x in ps], [x.clone() for x in m], [x.clone() for x in v]
+            torch_adam(ps, g, m, v, [], [torch.tensor(float(k)) for _ in ps], foreach=False, differentiable=True,
+                       amsgrad=False, beta1=h.b1, beta2=h.b2, lr=h.lr, weight_decay=0.0, eps=h.eps, maximize=False)
+        return torch.autograd.grad(sum(x.sum() for x in ps), p0)
+
+    res = {}
+    for name, fn in (("fused", fused), ("torch_op_by_op", reference)):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        res[name] = (time.perf_counter() - t0) / steps / K * 1e6
+    a = fused()
+    b = reference()
+    rel = float(max((torch.linalg.norm(x - y) / torch.linalg.norm(y)).item() for x, y in zip(a, b)))
+    return {"K": K, "leaves": len(shapes), "n_params": sum(int(torch.Size(s).numel()) for s in shapes),
+            "us_per_inner_step": {k: round(v, 1) for k, v in res.items()},
+            "speedup": round(res["torch_op_by_op"] / res["fused"], 2), "max_normrel_vs_torch": float("%.3g" % rel)}
+
+
 WORKLOAD_STEP = {
     "many_small_stepwise": "flatten p + K grads -> K single-step Adam fwd launches -> K single-step Adam bwd launches "
                            "-> unflatten p_K + K dg",
@@ -1059,7 +1122,22 @@ def main():
         w = WORKLOADS[{"many_small_treemap": "many_small", "sgd_flat": "many_small", "rmsprop_flat": "many_small",
                        "sgd_treemap": "many_small", "rmsprop_treemap": "many_small",
                        "es_resnet18": "resnet18_k1", "es_resnet18_noise": "resnet18_k1", "flat_1b_zero_mv": "flat_1b",
-                       "many_small_stepwise": "many_small", "small_trees": "tiny_mlp"}.get(a.workload, a.workload)]()
+                       "many_small_stepwise": "many_small", "small_trees": "tiny_mlp",
+                       "meta_loop": "tiny_mlp"}.get(a.workload, a.workload)]()
+    if a.workload == "meta_loop":
+        r = meta_loop(torch, P, max(a.steps, 20), max(a.warmup, 3))
+        print(json.dumps({
+            "metric": METRIC, "value": float("%.6g" % (r["n_params"] / (r["us_per_inner_step"]["fused"] * 1e-6))),
+            "unit": "params/s", "n_gpus": 1, "steps": max(a.steps, 20), "warmup": max(a.warmup, 3),
+            "ms_per_step": round(r["us_per_inner_step"]["fused"] * 1e-3, 6), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": "conv-net parameter tree (18 tensors, 112,261 params), K=5 inner steps through "
+                                   "AdamTreeFn and autograd (host path included), inner gradient of a quadratic "
+                                   "with create_graph; the same loop on torch.optim's functional Adam beside it",
+                       "launch": "eager", "parallelism": "single GPU"},
+            "meta_loop": r, "roofline": None, "cpu_baseline": None, "kernel_src_sha": kernel_source_sha()}),
+            flush=True)
+        return
     if a.workload == "small_trees":
         table = small_trees(torch, P, max(a.steps, 100), max(a.warmup, 5))
         t = table["tiny_mlp"]["leaf_direct_fused"]
