@@ -192,6 +192,33 @@ def test_es_rows_past_2_31_elements():
                      BWD_RTOL, "estimate")
 
 
+@pytest.mark.parametrize("n", [(1 << 31) + 8, BIG])
+def test_es_gaussian_past_2_31(n):
+    """In-kernel noise at a parameter count past 2^31 (n = 2^31 + 8 takes the
+    128-bit path, 2^31 + 7 the scalar one): perturbation and estimate on
+    sampled parameters against the oracle's noise for those columns."""
+    import paper_2211_06934_amd as P
+    N, sigma, seed = 2, 0.05, 0xB16B00B5
+    theta = torch_normal(n, 1.0, 42, "cuda")
+    out = torch.empty(2 * N, n, device="cuda")
+    P.es_perturb_gaussian(theta, N, seed, sigma, True, out)
+    f = torch.tensor([1.5, -0.25, 0.75, 2.0], device="cuda")
+    g = torch.empty(n, device="cuda")
+    P.es_estimate_gaussian(f, "antithetic", N, seed, sigma, g)
+    torch.cuda.synchronize()
+    idx = _index(n, 13)
+    ti = torch.from_numpy(idx).cuda()
+    ht = _take(theta, ti)
+    z, r = oracle.es_gaussian_noise_cols(N, idx, seed)
+    got = np.stack([_take(out[i], ti) for i in range(2 * N)])
+    mag = np.abs(ht)[None, :] + sigma * np.concatenate([r, r])
+    assert_mag_close(got, oracle.es_perturb(ht, z, sigma, True), mag, FWD_RTOL, "perturb")
+    hf = f.cpu().numpy()
+    w, scale = oracle.es_weights(hf, "antithetic", sigma)
+    mag = oracle.es_estimate_mag(r, oracle.es_weight_terms(hf, "antithetic"), scale)
+    assert_mag_close(_take(g, ti), oracle.es_estimate(z, w, scale), mag, BWD_RTOL, "estimate")
+
+
 def _end_to_end(h_p0, hG, h_cot, got_pK, got_muK, got_nuK, got_dg, got_dm0, got_dv0, er):
     """Against the all-fp64 oracle from the same fp32 inputs on the sampled
     elements: p_K within FWD_RTOL of its summed scales, the final moments and
