@@ -867,10 +867,11 @@ def log(msg):
     sys.stderr.flush()
 
 
-def time_workload(torch, P, S, step, phases, steps, warmup, graph=False):
+def time_workload(torch, P, S, step, phases, steps, warmup, graph=False, per_graph=1):
     """Warm up, then time `steps` steps: HIP events around every phase of every
-    step (eager), or around `steps` replays of one captured step (graph).
-    Returns (phase table, ms per step, per-phase ms or None)."""
+    step (eager), or around replays of a graph holding `per_graph` captured
+    steps, `steps` steps in all (graph).  Returns (phase table, ms per step,
+    per-phase ms or None)."""
     ph = phases(S)
     nph = len(ph)
     torch.cuda.synchronize()
@@ -888,14 +889,17 @@ def time_workload(torch, P, S, step, phases, steps, warmup, graph=False):
         torch.cuda.current_stream().wait_stream(side)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            step(P, S)
+            for _ in range(per_graph):
+                step(P, S)
         g.replay()
         torch.cuda.synchronize()
+        replays = max(1, steps // per_graph)
         t_start.record()
-        for _ in range(steps):
+        for _ in range(replays):
             g.replay()
         t_end.record()
         torch.cuda.synchronize()
+        return ph, t_start.elapsed_time(t_end) / (replays * per_graph), phase_ms
     else:
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nph + 1)] for _ in range(steps)]
         torch.cuda.synchronize()
@@ -996,11 +1000,42 @@ SMALL_FORMS = (
 )
 
 
+GRAPH_STEPS = 20  # steps captured per graph for the in-graph figure
+
+
+def graph_floor_us(torch, reps=200):
+    """Microseconds per replay of a graph holding one trivial kernel (a torch
+    add on 64 floats): the box's cost of a graph launch itself."""
+    x = torch.zeros(64, device="cuda")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        x.add_(1.0)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        x.add_(1.0)
+    for _ in range(20):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps * 1e3
+
+
 def small_trees(torch, P, steps, warmup):
     """The small trees (launch-bound) in three forms, each captured in a HIP
-    graph and replayed: microseconds per step and launches per step."""
+    graph and replayed: microseconds per step with one step per graph and with
+    GRAPH_STEPS steps per graph (the graph launch's own cost spread over
+    them), launches per step, and the box's replay cost of a one-kernel graph
+    for reference."""
     from workloads import WORKLOADS
-    table = {}
+    table = {"graph_floor_us": round(graph_floor_us(torch), 2)}
+    log("graph of one trivial kernel: %.2f us/replay" % table["graph_floor_us"])
     for wname in SMALL_TREES:
         w = WORKLOADS[wname]()
         row = {"n_params": w.n, "leaves": w.nseg, "K": w.K}
@@ -1013,9 +1048,14 @@ def small_trees(torch, P, steps, warmup):
                 S, step, phases = (setup_treemap(torch, P, w, "stored", stepwise=True), step_treemap_stepwise,
                                    phases_treemap_stepwise)
             ph, ms, _ = time_workload(torch, P, S, step, phases, steps, warmup, graph=True)
-            row[form] = {"us_per_step": round(ms * 1e3, 2), "launches_per_step": sum(p[2] for p in ph),
+            _, ms_g, _ = time_workload(torch, P, S, step, phases, max(steps, 5 * GRAPH_STEPS), warmup, graph=True,
+                                       per_graph=GRAPH_STEPS)
+            row[form] = {"us_per_step": round(ms * 1e3, 2),
+                         "us_per_step_%d_per_graph" % GRAPH_STEPS: round(ms_g * 1e3, 2),
+                         "launches_per_step": sum(p[2] for p in ph),
                          "G_params_per_s": round(w.n * w.K / (ms * 1e-3) / 1e9, 3)}
-            log("%s %s: %.2f us/step" % (wname, form, ms * 1e3))
+            log("%s %s: %.2f us/step (%.2f with %d steps per graph)" % (wname, form, ms * 1e3, ms_g * 1e3,
+                                                                       GRAPH_STEPS))
             del S
             torch.cuda.synchronize()
         table[wname] = row

@@ -271,7 +271,10 @@ int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
  *               accesses, others an element path with the same result
  * Aliasing as in the flat calls: an output leaf may be its own input leaf
  * (params_out[j] == params[j], dmu_in[j] == dmu[j], ...), never another leaf.
- * dmu and dnu are both NULL (zero cotangents) or both given.               */
+ * dmu and dnu are both NULL (zero cotangents) or both given.
+ * Small trees (at most 32 nonempty leaves and 65,536 elements) run one
+ * element per lane with the leaf table in the kernel arguments; the results
+ * are the same bit for bit.                                                */
 int diffopt_adam_fwd_tree(const diffopt_segtable* table, const uint64_t* params,
                           const uint64_t* grad, const uint64_t* mu,
                           const uint64_t* nu, int64_t count, double lr,

@@ -513,6 +513,116 @@ __global__ __launch_bounds__(kUBB) void adam_unrolled_bwd_elem(UBwdArgs a) {
     ubwd_element(e, a);
 }
 
+// ---- small buffers ---------------------------------------------------------------
+// Up to kSmallElems elements the fused launches are bound by latency, not
+// bandwidth: one element per lane (the shortest arithmetic chain per lane),
+// the step count a template argument so that every load of every step is
+// issued before the first step's arithmetic, and the kernel arguments
+// warmed at the start.  Same per-element arithmetic as the kernels above, so
+// the results agree bit for bit.
+constexpr int64_t kSmallElems = int64_t(1) << 16;
+constexpr int kSEB = 256;  // threads per workgroup of the small-buffer kernels
+
+template <int K>
+__global__ __launch_bounds__(kSEB) void adam_unrolled_fwd_small(UFwdArgs a) {
+  warm_args(fold_lines(a));
+  const int64_t e = (int64_t)blockIdx.x * kSEB + threadIdx.x;
+  if (e >= a.n) return;
+  float P = a.p[e], M = a.m0[e], V = a.v0[e];
+  float G[K];
+#pragma unroll
+  for (int s = 0; s < K; ++s) G[s] = a.g[s][e];
+#pragma unroll
+  for (int s = 0; s < K; ++s) {
+    const FwdOut o = fwd_elem(P, G[s], M, V, a.c[s]);
+    P = o.p;
+    M = o.m;
+    V = o.v;
+    if (a.m[s]) {  // uniform: a stored state
+      a.m[s][e] = M;
+      a.v[s][e] = V;
+    }
+  }
+  a.pK[e] = P;
+}
+
+// Stored states: launch step s is unrolled step khi - s (as in ubwd_element).
+// Without incoming moment cotangents their load slots read dP (unused), so
+// no load waits behind a branch.
+template <int K>
+__global__ __launch_bounds__(kSEB) void adam_unrolled_bwd_small(UBwdArgs a) {
+  warm_args(fold_lines(a));
+  const int64_t e = (int64_t)blockIdx.x * kSEB + threadIdx.x;
+  if (e >= a.n) return;
+  const float dP = a.dP[e];
+  const float dMi = (a.init_mv ? a.dm : a.dP)[e], dVi = (a.init_mv ? a.dv : a.dP)[e];
+  float G[K], M[K], V[K];
+#pragma unroll
+  for (int s = 0; s < K; ++s) {
+    G[s] = a.g[s][e];
+    M[s] = a.m[s][e];
+    V[s] = a.v[s][e];
+  }
+  float dM = dMi, dV = dVi;
+  BwdOut o = a.init_mv ? bwd_elem<true>(dP, dM, dV, G[0], M[0], V[0], a.c[0])
+                       : bwd_elem<false>(dP, 0.0f, 0.0f, G[0], M[0], V[0], a.c[0]);
+  a.dg[0][e] = o.g;
+  dM = o.m;
+  dV = o.v;
+#pragma unroll
+  for (int s = 1; s < K; ++s) {
+    o = bwd_elem<true>(dP, dM, dV, G[s], M[s], V[s], a.c[s]);
+    a.dg[s][e] = o.g;
+    dM = o.m;
+    dV = o.v;
+  }
+  a.dm[e] = dM;
+  a.dv[e] = dV;
+}
+
+template <int K>
+void launch_ufwd_small(const UFwdArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((adam_unrolled_fwd_small<K>), dim3((unsigned)((a.n + kSEB - 1) / kSEB)), dim3(kSEB), 0, st, a);
+}
+
+template <int K>
+void launch_ubwd_small(const UBwdArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((adam_unrolled_bwd_small<K>), dim3((unsigned)((a.n + kSEB - 1) / kSEB)), dim3(kSEB), 0, st, a);
+}
+
+// k in 1..kUK (16).
+template <class Args, template <int> class L>
+void dispatch_k(int k, const Args& a, hipStream_t st) {
+  switch (k) {
+    case 1: L<1>::run(a, st); break;
+    case 2: L<2>::run(a, st); break;
+    case 3: L<3>::run(a, st); break;
+    case 4: L<4>::run(a, st); break;
+    case 5: L<5>::run(a, st); break;
+    case 6: L<6>::run(a, st); break;
+    case 7: L<7>::run(a, st); break;
+    case 8: L<8>::run(a, st); break;
+    case 9: L<9>::run(a, st); break;
+    case 10: L<10>::run(a, st); break;
+    case 11: L<11>::run(a, st); break;
+    case 12: L<12>::run(a, st); break;
+    case 13: L<13>::run(a, st); break;
+    case 14: L<14>::run(a, st); break;
+    case 15: L<15>::run(a, st); break;
+    default: L<16>::run(a, st); break;
+  }
+}
+static_assert(kUK == 16, "dispatch_k instantiates 1..16 steps");
+
+template <int K>
+struct FwdSmall {
+  static void run(const UFwdArgs& a, hipStream_t st) { launch_ufwd_small<K>(a, st); }
+};
+template <int K>
+struct BwdSmall {
+  static void run(const UBwdArgs& a, hipStream_t st) { launch_ubwd_small<K>(a, st); }
+};
+
 // ---- fused K-step VJP over a run of steps whose moments were not stored -------------
 // For a run of C steps j+1..j+C of which only the state (mu_j, nu_j) before
 // the first was stored, the lane reads that state and the C gradients once,
@@ -613,6 +723,39 @@ __device__ __forceinline__ void urbwd_element(int64_t e, const URBwdArgs& a) {
   a.dv[e] = dV;
 }
 
+// Small buffers (see adam_unrolled_fwd_small): the arithmetic of urbwd_element.
+template <int C>
+__global__ __launch_bounds__(kSEB) void adam_unrolled_bwd_remat_small(URBwdArgs a) {
+  warm_args(fold_lines(a));
+  const int64_t e = (int64_t)blockIdx.x * kSEB + threadIdx.x;
+  if (e >= a.n) return;
+  const float dP = a.dP[e];
+  const float dMi = (a.init_mv ? a.dm : a.dP)[e], dVi = (a.init_mv ? a.dv : a.dP)[e];
+  float G[C], M[C], V[C];
+  M[0] = a.m0[e];
+  V[0] = a.v0[e];
+#pragma unroll
+  for (int s = 0; s < C; ++s) G[s] = a.g[s][e];
+#pragma unroll
+  for (int s = 0; s + 1 < C; ++s) {
+    M[s + 1] = moment1(G[s], M[s], a.c[s]);
+    V[s + 1] = moment2(G[s], V[s], a.c[s]);
+  }
+  BwdOut o = a.init_mv ? bwd_elem<true>(dP, dMi, dVi, G[C - 1], M[C - 1], V[C - 1], a.c[C - 1])
+                       : bwd_elem<false>(dP, 0.0f, 0.0f, G[C - 1], M[C - 1], V[C - 1], a.c[C - 1]);
+  a.dg[C - 1][e] = o.g;
+  float dM = o.m, dV = o.v;
+#pragma unroll
+  for (int s = C - 2; s >= 0; --s) {
+    o = bwd_elem<true>(dP, dM, dV, G[s], M[s], V[s], a.c[s]);
+    a.dg[s][e] = o.g;
+    dM = o.m;
+    dV = o.v;
+  }
+  a.dm[e] = dM;
+  a.dv[e] = dV;
+}
+
 template <int C, int B>
 __global__ __launch_bounds__(B) void adam_unrolled_bwd_remat_vec(URBwdArgs a) {
   const int64_t nv = a.n >> 2;
@@ -639,7 +782,10 @@ template <int C>
 void launch_urbwd(bool vec, const URBwdArgs& a, hipStream_t st) {
   constexpr int B = C >= DIFFOPT_URBWD_LONG_RUN ? DIFFOPT_URBWD_BLOCK_LONG : kURB;
   constexpr int BS = B < kSmallB ? B : kSmallB;
-  if (vec && (a.n >> 2) < kSmallVecs)
+  if (a.n <= kSmallElems)
+    hipLaunchKernelGGL((adam_unrolled_bwd_remat_small<C>), dim3((unsigned)((a.n + kSEB - 1) / kSEB)), dim3(kSEB), 0,
+                       st, a);
+  else if (vec && (a.n >> 2) < kSmallVecs)
     hipLaunchKernelGGL((adam_unrolled_bwd_remat_vec<C, BS>), dim3((unsigned)grid_for(((a.n >> 2) + BS - 1) / BS)),
                        dim3(BS), 0, st, a);
   else if (vec)
@@ -821,7 +967,9 @@ extern "C" int diffopt_adam_unrolled_fwd(int64_t K, int64_t n, const float* p0, 
       a.m[a.K - 1] = mu_traj[K];
       a.v[a.K - 1] = nu_traj[K];
     }
-    if (vec && (n >> 2) < kSmallVecs)
+    if (n <= kSmallElems)
+      dispatch_k<UFwdArgs, FwdSmall>(a.K, a, st);
+    else if (vec && (n >> 2) < kSmallVecs)
       hipLaunchKernelGGL((adam_unrolled_fwd_vec<kSmallB>), dim3((unsigned)grid_for(((n >> 2) + kSmallB - 1) / kSmallB)),
                          dim3(kSmallB), 0, st, a);
     else if (vec)
@@ -887,7 +1035,9 @@ extern "C" int diffopt_adam_unrolled_bwd(int64_t K, int64_t n, const float* dpK,
         if (on) make_coef(who, count0 + k - 1, lr, b1, b2, eps, eps_root, &a.c[s]);
         else a.c[s] = AdamCoef{};
       }
-      if (vec && (n >> 2) < kSmallVecs)
+      if (n <= kSmallElems)
+        dispatch_k<UBwdArgs, BwdSmall>(a.K, a, st);
+      else if (vec && (n >> 2) < kSmallVecs)
         hipLaunchKernelGGL((adam_unrolled_bwd_vec<kSmallB>),
                            dim3((unsigned)grid_for(((n >> 2) + kSmallB - 1) / kSmallB)), dim3(kSmallB), 0, st, a);
       else if (vec)

@@ -59,6 +59,22 @@ struct SegEntry {
   int64_t orig;   // index into the caller's leaf-address array
 };
 
+// Small trees: the table of nonempty leaves, passed to the leaf-direct Adam
+// kernels by value so that a lane finds its leaf from kernel arguments alone.
+// Lane j takes element j of the concatenated leaves (no group padding).  The
+// launch is then bound by dependent memory latency and by each lane's chain
+// of arithmetic rather than by bandwidth, so each lane takes one element and
+// issues every load before any arithmetic.
+constexpr int kTinyLeaves = 32;
+constexpr int64_t kTinyElems = int64_t(1) << 16;
+
+struct TinyTable {
+  int32_t n = 0;                 // nonempty leaves
+  int32_t total = 0;             // their element count
+  int32_t start[kTinyLeaves]{};  // first element of each leaf; INT32_MAX past the last leaf
+  int32_t orig[kTinyLeaves]{};   // the leaf's index in the caller's leaf-address arrays
+};
+
 }  // namespace diffopt
 
 struct diffopt_segtable {
@@ -70,6 +86,8 @@ struct diffopt_segtable {
   int32_t elem_bytes = 4;
   int device = 0;
   int dense_orig = 1;               // no empty leaves: table index == leaf index
+  int tiny = 0;                     // the leaves fit a TinyTable (held in `small`)
+  diffopt::TinyTable small;
   diffopt::SegEntry* d_seg = nullptr;       // [nact + 1]
   int64_t* d_tile_first = nullptr;  // [ntiles + 1]
 };

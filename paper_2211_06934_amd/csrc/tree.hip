@@ -281,6 +281,19 @@ extern "C" int diffopt_segtable_create(int64_t nseg, const int64_t* numel, const
   t->ntiles = (goff + kTileGroups - 1) / kTileGroups;
   t->dense_orig = (nact == nseg) ? 1 : 0;
   if (hipGetDevice(&t->device) != hipSuccess) t->device = -1;
+  int64_t elems = 0;
+  for (int64_t j = 0; j < nact; ++j) elems += host[(size_t)j].numel;
+  if (nact >= 1 && nact <= kTinyLeaves && elems <= kTinyElems) {
+    t->tiny = 1;
+    t->small.n = (int32_t)nact;
+    int32_t at = 0;
+    for (int64_t j = 0; j < kTinyLeaves; ++j) {
+      t->small.start[j] = j < nact ? at : INT32_MAX;
+      t->small.orig[j] = j < nact ? (int32_t)host[(size_t)j].orig : 0;
+      if (j < nact) at += (int32_t)host[(size_t)j].numel;
+    }
+    t->small.total = at;
+  }
 
   std::vector<int64_t> tf;
   if (t->ntiles > 0) {

@@ -593,6 +593,194 @@ int launch_trbwd_c(const char* who, int C, const diffopt_segtable* t, const TRBw
 }
 static_assert(kTRS == 8, "launch_trbwd_c instantiates run lengths 1..8");
 
+// ---- small trees ------------------------------------------------------------------
+// When the leaves fit a TinyTable the fused steps run one element per lane
+// with the table in kernel arguments (no staged window, no barrier): a lane
+// finds its leaf by a scan over the table, loads its leaf's address in every
+// operand, then every input of every step, and only then computes.  The
+// arithmetic per element is that of the kernels above, so the results are
+// the same bit for bit.  Measured on MI355X for the 1,761-parameter tree at
+// K = 5: about 7.4 and 8.2 us per fused forward and VJP launch through the
+// staged window (each step a serial load and a four-element arithmetic chain
+// per lane), which this form shortens to the latency of two dependent loads
+// and one element's chain.
+constexpr int kTinyB = 256;
+
+// Element j of the concatenated leaves: its leaf's caller index and its index
+// in the leaf.  The scan is unrolled over the whole table (entries past the
+// last leaf start at INT32_MAX), so it reads the kernel arguments at fixed
+// offsets and takes no branch.  Each entry passes through an empty asm
+// statement so that it is selected as a value held in a scalar register:
+// otherwise the compiler selects its address instead and reads the chosen
+// entry with a per-lane load, one more memory round trip before the leaf
+// addresses can be loaded.
+__device__ __forceinline__ bool tiny_slot(const TinyTable& tt, int64_t j, int& orig, int64_t& i) {
+  if (j >= tt.total) return false;
+  const int32_t jj = (int32_t)j;
+  int o = tt.orig[0];
+  int32_t first = 0;
+#pragma unroll
+  for (int t = 1; t < kTinyLeaves; ++t) {
+    int32_t st = tt.start[t], ot = tt.orig[t];
+    asm volatile("" : "+s"(st), "+s"(ot));
+    const bool in = jj >= st;
+    o = in ? ot : o;
+    first = in ? st : first;
+  }
+  orig = o;
+  i = jj - first;
+  return true;
+}
+
+// Leaf addresses as global-space pointers (see gptr): every load below is then
+// a global_* instruction, counted by the vector-memory counter alone.
+__device__ __forceinline__ gptr<const float> leaf_in(const uint64_t* arr, int orig) {
+  return gaddr<const float>(arr[orig]);
+}
+__device__ __forceinline__ gptr<float> leaf_out(const uint64_t* arr, int orig) {
+  return gaddr<float>(arr[orig]);
+}
+
+// The fused forward over K <= kTK steps (operands as in TFwdArgs, a.K == K).
+// Every address and every input is loaded before the first step; an unstored
+// step state takes the address of pK for its (unused) load slot, so no load
+// waits behind a branch.
+template <int K>
+__global__ __launch_bounds__(kTinyB) void adam_unrolled_fwd_tree_tiny(TinyTable tt, TFwdArgs a) {
+  warm_args(fold_lines(tt) ^ fold_lines(a));
+  int leaf;
+  int64_t i;
+  if (!tiny_slot(tt, (int64_t)blockIdx.x * kTinyB + threadIdx.x, leaf, i)) return;
+  const auto P0 = leaf_in(a.a[0], leaf);
+  const auto M0 = leaf_in(a.a[1], leaf);
+  const auto V0 = leaf_in(a.a[2], leaf);
+  const auto PK = leaf_out(a.a[3], leaf);
+  gptr<const float> Gp[K];
+  gptr<float> Mo[K], Vo[K];
+#pragma unroll
+  for (int s = 0; s < K; ++s) {
+    Gp[s] = leaf_in(a.a[4 + 3 * s], leaf);
+    const bool kept = a.a[5 + 3 * s] != nullptr;  // uniform: a stored state
+    Mo[s] = leaf_out(kept ? a.a[5 + 3 * s] : a.a[3], leaf);
+    Vo[s] = leaf_out(kept ? a.a[6 + 3 * s] : a.a[3], leaf);
+  }
+  float p = P0[i], m = M0[i], v = V0[i];
+  float G[K];
+#pragma unroll
+  for (int s = 0; s < K; ++s) G[s] = Gp[s][i];
+#pragma unroll
+  for (int s = 0; s < K; ++s) {
+    const FwdOut o = fwd_elem(p, G[s], m, v, a.c[s]);
+    p = o.p;
+    m = o.m;
+    v = o.v;
+    if (a.a[5 + 3 * s]) {
+      Mo[s][i] = m;
+      Vo[s][i] = v;
+    }
+  }
+  PK[i] = p;
+}
+
+// The VJP over a run of C steps from one stored state (mu_j, nu_j), last step
+// first, as adam_unrolled_bwd_tree_remat_kernel; the incoming and outgoing
+// moment cotangents have their own operands so that the single-step VJP (C =
+// 1, separate input and output trees) takes the same kernel.
+constexpr int kTinyBwdNA = 7 + 2 * kTRS;  // 0 dP, 1 dM in, 2 dV in, 3 dM out, 4 dV out, 5 mu_j, 6 nu_j;
+                                          // per step s: 7+2s g, 8+2s dg
+struct TinyBwdArgs {
+  const uint64_t* a[kTinyBwdNA];
+  AdamCoef c[kTRS];
+  int32_t init_mv;  // 0: zero dM, dV before the run's last step (operands 1, 2 unused)
+};
+
+template <int C>
+__global__ __launch_bounds__(kTinyB) void adam_unrolled_bwd_tree_tiny(TinyTable tt, TinyBwdArgs a) {
+  warm_args(fold_lines(tt) ^ fold_lines(a));
+  int leaf;
+  int64_t i;
+  if (!tiny_slot(tt, (int64_t)blockIdx.x * kTinyB + threadIdx.x, leaf, i)) return;
+  // without incoming moment cotangents their load slots read dP (unused)
+  const auto DP = leaf_in(a.a[0], leaf);
+  const auto DMi = leaf_in(a.init_mv ? a.a[1] : a.a[0], leaf);
+  const auto DVi = leaf_in(a.init_mv ? a.a[2] : a.a[0], leaf);
+  const auto DMo = leaf_out(a.a[3], leaf);
+  const auto DVo = leaf_out(a.a[4], leaf);
+  const auto Mj = leaf_in(a.a[5], leaf);
+  const auto Vj = leaf_in(a.a[6], leaf);
+  gptr<const float> Gp[C];
+  gptr<float> DG[C];
+#pragma unroll
+  for (int s = 0; s < C; ++s) {
+    Gp[s] = leaf_in(a.a[7 + 2 * s], leaf);
+    DG[s] = leaf_out(a.a[8 + 2 * s], leaf);
+  }
+  const float dP = DP[i];
+  const float dMi = DMi[i], dVi = DVi[i];
+  float G[C], M[C], V[C];
+  M[0] = Mj[i];
+  V[0] = Vj[i];
+#pragma unroll
+  for (int s = 0; s < C; ++s) G[s] = Gp[s][i];
+  float dM = a.init_mv ? dMi : 0.0f, dV = a.init_mv ? dVi : 0.0f;
+#pragma unroll
+  for (int s = 0; s + 1 < C; ++s) {
+    M[s + 1] = moment1(G[s], M[s], a.c[s]);
+    V[s + 1] = moment2(G[s], V[s], a.c[s]);
+  }
+#pragma unroll
+  for (int s = C - 1; s >= 0; --s) {
+    const BwdOut o = (s == C - 1 && !a.init_mv) ? bwd_elem<false>(dP, 0.0f, 0.0f, G[s], M[s], V[s], a.c[s])
+                                                : bwd_elem<true>(dP, dM, dV, G[s], M[s], V[s], a.c[s]);
+    DG[s][i] = o.g;
+    dM = o.m;
+    dV = o.v;
+  }
+  DMo[i] = dM;
+  DVo[i] = dV;
+}
+
+unsigned tiny_blocks(const diffopt_segtable* t) { return (unsigned)((t->small.total + kTinyB - 1) / kTinyB); }
+
+template <int K>
+void launch_tiny_fwd(const diffopt_segtable* t, const TFwdArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((adam_unrolled_fwd_tree_tiny<K>), dim3(tiny_blocks(t)), dim3(kTinyB), 0, st, t->small, a);
+}
+
+void launch_tiny_fwd_k(const diffopt_segtable* t, const TFwdArgs& a, hipStream_t st) {
+  switch (a.K) {  // 1 <= a.K <= kTK
+    case 1: launch_tiny_fwd<1>(t, a, st); break;
+    case 2: launch_tiny_fwd<2>(t, a, st); break;
+    case 3: launch_tiny_fwd<3>(t, a, st); break;
+    case 4: launch_tiny_fwd<4>(t, a, st); break;
+    case 5: launch_tiny_fwd<5>(t, a, st); break;
+    case 6: launch_tiny_fwd<6>(t, a, st); break;
+    case 7: launch_tiny_fwd<7>(t, a, st); break;
+    default: launch_tiny_fwd<8>(t, a, st); break;
+  }
+}
+static_assert(kTK == 8, "launch_tiny_fwd_k instantiates 1..8 steps");
+
+template <int C>
+void launch_tiny_bwd(const diffopt_segtable* t, const TinyBwdArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((adam_unrolled_bwd_tree_tiny<C>), dim3(tiny_blocks(t)), dim3(kTinyB), 0, st, t->small, a);
+}
+
+int launch_tiny_bwd_c(const char* who, int C, const diffopt_segtable* t, const TinyBwdArgs& a, hipStream_t st) {
+  switch (C) {
+    case 1: launch_tiny_bwd<1>(t, a, st); break;
+    case 2: launch_tiny_bwd<2>(t, a, st); break;
+    case 3: launch_tiny_bwd<3>(t, a, st); break;
+    case 4: launch_tiny_bwd<4>(t, a, st); break;
+    case 5: launch_tiny_bwd<5>(t, a, st); break;
+    case 6: launch_tiny_bwd<6>(t, a, st); break;
+    case 7: launch_tiny_bwd<7>(t, a, st); break;
+    case 8: launch_tiny_bwd<8>(t, a, st); break;
+    default: return fail(DIFFOPT_EINVAL, "%s: recompute run of %d steps (at most %d)", who, C, kTRS);
+  }
+  return DIFFOPT_OK;
+}
+
 // ---- leaf-direct SGD-momentum and RMSProp ------------------------------------------
 // The ops of optim_ops.hpp applied leaf by leaf, in the layout of the fused
 // Adam kernels: one table tile per workgroup, one group per lane, the leaf
@@ -707,6 +895,20 @@ extern "C" int diffopt_adam_fwd_tree(const diffopt_segtable* table, const uint64
   if (table->ntiles == 0) return DIFFOPT_OK;
   if (!params || !grad || !mu || !nu || !params_out || !mu_out || !nu_out)
     return fail(DIFFOPT_EINVAL, "%s: null leaf-address array", who);
+  if (table->tiny) {  // the fused forward at K = 1, its step state stored in the outputs
+    TFwdArgs a{};
+    a.K = 1;
+    a.a[0] = params;
+    a.a[1] = mu;
+    a.a[2] = nu;
+    a.a[3] = params_out;
+    a.a[4] = grad;
+    a.a[5] = mu_out;
+    a.a[6] = nu_out;
+    a.c[0] = c;
+    launch_tiny_fwd<1>(table, a, as_stream(stream));
+    return launch_status(who);
+  }
   const LeafArrays<7> arr{{params, grad, mu, nu, params_out, mu_out, nu_out}};
   return launch_fwd_tree(table, arr, c, as_stream(stream));
 }
@@ -728,6 +930,22 @@ extern "C" int diffopt_adam_bwd_tree(const diffopt_segtable* table, const uint64
   if (table->ntiles == 0) return DIFFOPT_OK;
   if (!dupdate || !grad || !mu || !nu || !dgrad || !dmu_in || !dnu_in)
     return fail(DIFFOPT_EINVAL, "%s: null leaf-address array", who);
+  if (table->tiny) {  // the recomputing VJP over one step from the stored (mu, nu)
+    TinyBwdArgs a{};
+    a.init_mv = dmu != nullptr;
+    a.a[0] = dupdate;
+    a.a[1] = dmu;
+    a.a[2] = dnu;
+    a.a[3] = dmu_in;
+    a.a[4] = dnu_in;
+    a.a[5] = mu;
+    a.a[6] = nu;
+    a.a[7] = grad;
+    a.a[8] = dgrad;
+    a.c[0] = c;
+    launch_tiny_bwd<1>(table, a, as_stream(stream));
+    return launch_status(who);
+  }
   const LeafArrays<9> arr{{dupdate, dmu, dnu, grad, mu, nu, dgrad, dmu_in, dnu_in}};
   return launch_bwd_tree(table, arr, c, as_stream(stream));
 }
@@ -774,9 +992,13 @@ extern "C" int diffopt_adam_unrolled_fwd_tree(const diffopt_segtable* table, int
       a.a[5 + 3 * (a.K - 1)] = mu_traj[K];
       a.a[6 + 3 * (a.K - 1)] = nu_traj[K];
     }
-    const size_t lds = sizeof(uint64_t) * kWindowMax * (4 + 3 * a.K);
-    hipLaunchKernelGGL(adam_unrolled_fwd_tree_kernel, dim3((unsigned)table->ntiles), dim3(kUTB), lds, st,
-                       table->d_seg, table->d_tile_first, table->ngroups, table->dense_orig, a);
+    if (table->tiny) {
+      launch_tiny_fwd_k(table, a, st);
+    } else {
+      const size_t lds = sizeof(uint64_t) * kWindowMax * (4 + 3 * a.K);
+      hipLaunchKernelGGL(adam_unrolled_fwd_tree_kernel, dim3((unsigned)table->ntiles), dim3(kUTB), lds, st,
+                         table->d_seg, table->d_tile_first, table->ngroups, table->dense_orig, a);
+    }
     rc = launch_status(who);
     if (rc) return rc;
   }
@@ -814,9 +1036,28 @@ extern "C" int diffopt_adam_unrolled_bwd_tree(const diffopt_segtable* table, int
   for (int64_t khi = K; khi >= 1;) {
     const int32_t init_mv = khi != K;  // the first launch starts from zero cotangents of mu_K, nu_K
     if (mu_traj[khi - 1]) {
-      TBwdArgs a{};
       int32_t run = 0;
       while (run < kTK && khi - run >= 1 && mu_traj[khi - run - 1]) ++run;
+      if (table->tiny && run == 1) {  // one step from its stored state: the small form at C = 1
+        TinyBwdArgs a{};
+        a.init_mv = init_mv;
+        a.a[0] = dpK;
+        a.a[1] = dmu0;
+        a.a[2] = dnu0;
+        a.a[3] = dmu0;
+        a.a[4] = dnu0;
+        a.a[5] = mu_traj[khi - 1];
+        a.a[6] = nu_traj[khi - 1];
+        a.a[7] = grads[khi - 1];
+        a.a[8] = dgrads[khi - 1];
+        make_coef(who, count0 + khi - 1, lr, b1, b2, eps, eps_root, &a.c[0]);
+        launch_tiny_bwd<1>(table, a, st);
+        khi -= 1;
+        rc = launch_status(who);
+        if (rc) return rc;
+        continue;
+      }
+      TBwdArgs a{};
       a.K = run;
       a.init_mv = init_mv;
       a.a[0] = dpK;
@@ -838,6 +1079,28 @@ extern "C" int diffopt_adam_unrolled_bwd_tree(const diffopt_segtable* table, int
       int64_t j = khi - 1;
       while (!mu_traj[j]) --j;  // mu_traj[0] is stored; check_trajectory bounds khi - j by kTRS
       const int C = (int)(khi - j);
+      if (table->tiny) {
+        TinyBwdArgs a{};
+        a.init_mv = init_mv;
+        a.a[0] = dpK;
+        a.a[1] = dmu0;
+        a.a[2] = dnu0;
+        a.a[3] = dmu0;
+        a.a[4] = dnu0;
+        a.a[5] = mu_traj[j];
+        a.a[6] = nu_traj[j];
+        for (int s = 0; s < C; ++s) {
+          a.a[7 + 2 * s] = grads[j + s];
+          a.a[8 + 2 * s] = dgrads[j + s];
+          make_coef(who, count0 + j + s, lr, b1, b2, eps, eps_root, &a.c[s]);
+        }
+        rc = launch_tiny_bwd_c(who, C, table, a, st);
+        if (rc) return rc;
+        khi = j;
+        rc = launch_status(who);
+        if (rc) return rc;
+        continue;
+      }
       TRBwdArgs a{};
       a.init_mv = init_mv;
       a.a[0] = dpK;

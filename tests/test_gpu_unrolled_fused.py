@@ -97,6 +97,11 @@ CASES = [  # K, n, count0, eps_root, nonzero initial state
     (16, 12289, 0, 0.0, False),
     (17, 12290, 3, 1e-8, True),
     (33, 5003, 0, 0.0, True),
+    # above 2^16 elements the tiled kernels run (below, one element per lane)
+    (3, 1 << 16, 0, 0.0, False),
+    (3, (1 << 16) + 1, 0, 1e-8, True),
+    (5, (1 << 16) + 4097 * 4 + 3, 100, 1e-8, True),
+    (17, 70002, 3, 1e-8, True),
 ]
 
 
@@ -116,10 +121,11 @@ def test_fused_equals_stepwise_bitwise(K, n, count0, er, nz):
     _assert_same(got[5], ref[5], "dnu0")
 
 
+@pytest.mark.parametrize("n", [3 * 4096 + 5, (1 << 16) + 3 * 4096 + 5])
 @pytest.mark.parametrize("offset", [1, 4])
 @pytest.mark.parametrize("in_place", [False, True])
-def test_misaligned_and_in_place_equal_fused(offset, in_place):
-    K, n = 4, 3 * 4096 + 5
+def test_misaligned_and_in_place_equal_fused(offset, in_place, n):
+    K = 4
     inp = _inputs(K, n, 11, True)
     ref = _fused(*inp, 0, 1e-8)
     got = _fused(*inp, 0, 1e-8, in_place=in_place, offset=offset)

@@ -97,6 +97,11 @@ CASES = [  # K, n, count0, eps_root, nonzero initial state, store policy
     (20, 5003, 1, 1e-8, True, 3),
     (40, 2049, 0, 0.0, False, (7, 14, 21, 28, 35)),  # states 16 and 32 unstored
     (33, 1025, 5, 0.0, True, (1, 2, 9, 10, 11, 18, 25, 32)),  # stored runs and recomputed runs mixed
+    # above 2^16 elements the tiled kernels run (below, one element per lane)
+    (8, 1 << 16, 0, 0.0, False, "none"),
+    (5, (1 << 16) + 1, 7, 0.0, True, "none"),
+    (17, 70003, 0, 1e-8, False, (3, 10)),
+    (20, (1 << 16) + 5003, 1, 1e-8, True, 3),
 ]
 
 
@@ -109,14 +114,14 @@ def test_recomputed_trajectory_equals_stored_bitwise(K, n, count0, er, nz, polic
     _compare(got, ref, K)
 
 
+@pytest.mark.parametrize("n", [3 * 4096 + 5, (1 << 16) + 3 * 4096 + 5])
 @pytest.mark.parametrize("offset", [1, 4])
 @pytest.mark.parametrize("in_place", [False, True])
 @pytest.mark.parametrize("K,policy", [(6, (2,)), (19, (4, 11, 18))])
-def test_recomputed_misaligned_and_in_place(offset, in_place, K, policy):
+def test_recomputed_misaligned_and_in_place(offset, in_place, K, policy, n):
     # K = 19: state 16 is not stored, so the running moments cross the
     # forward's launch boundary through the final-state buffers (element
-    # kernels when offset is not a multiple of 4)
-    n = 3 * 4096 + 5
+    # kernels when offset is not a multiple of 4 and n is above 2^16)
     inp = _inputs(K, n, 17, True)
     ref = _run(*inp, 0, 1e-8, "all")
     got = _run(*inp, 0, 1e-8, policy, in_place=in_place, offset=offset)
