@@ -110,7 +110,12 @@ struct CopyBatch {
 // fetches 1.019 of the algorithmic bytes against 1.042 for the plain order
 // (the rest is the table and the partial head/tail groups), at the same or
 // slightly better rate (pack 6.12 against 6.10 TB/s, unpack 6.24 against
-// 6.22, six paired allocations); R = 2 fell in between.
+// 6.22, six paired allocations); R = 2 fell in between.  A workgroup that
+// copies a run of 2, 4 or 8 tiles in turn, with the next window prefetched,
+// was slower (pack 5.1, 4.7, 4.6 TB/s against 6.1): the memory counter
+// retires in order and counts stores too, so each tile's loads wait for the
+// previous tile's stores, where one-tile workgroups end with their stores in
+// flight.
 #ifndef DIFFOPT_TREE_RUN
 #define DIFFOPT_TREE_RUN 4
 #endif
