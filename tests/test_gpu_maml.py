@@ -57,9 +57,9 @@ def _task(seed, n=25):
     return xs, ys, xq, yq
 
 
-def _meta_grad_ours(init, task, K, device, conv_bias=False):
+def _meta_grad_ours(init, task, K, device, conv_bias=False, width=64):
     import paper_2211_06934_amd as P
-    net = ConvNet(conv_bias=conv_bias).to(device)
+    net = ConvNet(width=width, conv_bias=conv_bias).to(device)
     with torch.no_grad():
         for n, p in net.named_parameters():
             p.copy_(init[n])
@@ -187,23 +187,26 @@ def _recording_adam_tree_fn(log):
     return Rec
 
 
-@pytest.mark.parametrize("K,conv_bias", [(1, False), (3, False), (2, True)])
-def test_maml_fused_steps_match_oracle_inside_the_loop(K, conv_bias, monkeypatch):
+@pytest.mark.parametrize("K,conv_bias,width", [(1, False, 64), (3, False, 64), (2, True, 64),
+                                               (3, False, 16), (2, True, 16)])
+def test_maml_fused_steps_match_oracle_inside_the_loop(K, conv_bias, width, monkeypatch):
     # Every fused step the real MAML loop runs -- warm moments after step 1,
     # cotangents that carry the model's Hessian-vector products into the
     # earlier steps, and (conv_bias) zero-gradient leaves at the 0/0 point
     # mixed with live ones -- checked element by element against the oracle
     # on the inputs that step actually received: 1e-5 of the term scale for
     # the forward, 1e-4 for the VJP, and the params cotangent passed through
-    # bit for bit.
+    # bit for bit.  Width 64 (112,261 parameters) takes the tiled leaf-direct
+    # kernels, width 16 (14 or 18 leaves, about 7,300 parameters) the
+    # small-tree kernels.
     import oracle
     import paper_2211_06934_amd as P
     from tests.support import BWD_RTOL, FWD_RTOL, assert_mag_close
     log = []
     monkeypatch.setattr(P.autograd, "AdamTreeFn", _recording_adam_tree_fn(log))
     torch.manual_seed(2 + K)
-    init = {n: p.detach().clone() for n, p in ConvNet(conv_bias=conv_bias).named_parameters()}
-    grads, outer = _meta_grad_ours(init, _task(7 + K), K, "cuda", conv_bias=conv_bias)
+    init = {n: p.detach().clone() for n, p in ConvNet(width=width, conv_bias=conv_bias).named_parameters()}
+    grads, outer = _meta_grad_ours(init, _task(7 + K), K, "cuda", conv_bias=conv_bias, width=width)
     assert np.isfinite(outer) and all(torch.isfinite(g).all() for g in grads)
     fw = [r for r in log if r["kind"] == "fwd"]
     bw = [r for r in log if r["kind"] == "bwd"]
@@ -229,7 +232,8 @@ def test_maml_fused_steps_match_oracle_inside_the_loop(K, conv_bias, monkeypatch
         assert np.array_equal(r["res"][0], dP), "params cotangent is the identity"
         for name, got, x, mg in zip(("dg", "dm", "dv"), r["res"][1:], ref[1:], mag):
             assert_mag_close(got, x, mg, BWD_RTOL, "VJP step %d %s" % (r["count"], name))
-    print("K=%d conv_bias=%s: %d gradient elements exactly 0, %d below 1e-8" % (K, conv_bias, zero_g, tiny_g))
+    print("K=%d conv_bias=%s width=%d: %d gradient elements exactly 0, %d below 1e-8" % (K, conv_bias, width, zero_g,
+                                                                                   tiny_g))
     if conv_bias:
         # the biases in front of batch normalisation have a gradient that is
         # zero in exact arithmetic and at rounding level in fp32: the loop
