@@ -106,18 +106,20 @@ struct CopyBatch {
 // R > 1, each block of 8R workgroups takes 8R consecutive tiles so that the R
 // workgroups an XCD receives get R consecutive tiles (the chip still works
 // through one 8R-tile block at a time); a ragged last block keeps the plain
-// order.  Measured on the 20,000-leaf tree, four trees per launch: R = 4
-// fetches 1.019 of the algorithmic bytes against 1.042 for the plain order
-// (the rest is the table and the partial head/tail groups), at the same or
-// slightly better rate (pack 6.12 against 6.10 TB/s, unpack 6.24 against
-// 6.22, six paired allocations); R = 2 fell in between.  A workgroup that
+// order.  Measured on the 20,000-leaf tree, four trees per launch, fetched
+// bytes over algorithmic (pack / unpack): plain order 1.042, R = 4 1.020 /
+// 1.018, R = 8 1.014 / 1.012, R = 16 1.011 / 1.008, R = 32 1.009 / 1.006,
+// R = 64 1.008 / 1.005 (the rest is the table and the partial head/tail
+// groups).  The rate is the same within noise up to R = 32 (paired runs:
+// R = 4 pack 6.12 against 6.10 TB/s for the plain order; R = 32 5.96 against
+// 5.99 for R = 16 on a slower box) and 1% lower at R = 64.  A workgroup that
 // copies a run of 2, 4 or 8 tiles in turn, with the next window prefetched,
 // was slower (pack 5.1, 4.7, 4.6 TB/s against 6.1): the memory counter
 // retires in order and counts stores too, so each tile's loads wait for the
 // previous tile's stores, where one-tile workgroups end with their stores in
 // flight.
 #ifndef DIFFOPT_TREE_RUN
-#define DIFFOPT_TREE_RUN 4
+#define DIFFOPT_TREE_RUN 32
 #endif
 
 __device__ __forceinline__ int64_t tree_tile(int64_t b, int64_t ntiles) {
