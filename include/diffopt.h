@@ -107,7 +107,10 @@ int64_t diffopt_segtable_nseg(const diffopt_segtable* table);
  *   flat        device buffer of at least diffopt_segtable_total() elements
  * Copies bits through integer registers: NaN payloads, signed zeros and
  * subnormals survive.  Pointers must be aligned to elem_bytes.  The flat
- * buffer must not overlap any leaf.                                         */
+ * buffer must not overlap any leaf.  Small tables (at most 32 nonempty
+ * leaves and 65,536 elements, laid out as the plain concatenation of the
+ * leaves) are copied one element per lane with the table in the kernel
+ * arguments; the result is the same.                                       */
 int diffopt_tree_flatten(const diffopt_segtable* table,
                          const uint64_t* leaf_ptrs, void* flat, void* stream);
 

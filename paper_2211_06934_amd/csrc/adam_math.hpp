@@ -116,26 +116,6 @@ __device__ __forceinline__ void st(__attribute__((address_space(1))) T* p, T v) 
 #endif
 }
 
-// ---- kernel arguments of the small-problem kernels ---------------------------
-// Kernel arguments are read through the scalar cache, one 64-byte line at a
-// time, and the compiler loads each step's coefficients just before that
-// step: in a kernel bound by latency every step then waits for a memory
-// round trip of its own (about 0.4 us per step on MI355X).  Folding one word
-// of every line of an argument into a single value that an empty asm
-// statement consumes makes the kernel issue all of those loads at its start,
-// with one wait; the later reads of the same lines hit the cache.
-template <class T>
-__device__ __forceinline__ int32_t fold_lines(const T& x) {
-  constexpr int kWords = (int)(sizeof(T) / 4);
-  const int32_t* w = reinterpret_cast<const int32_t*>(&x);
-  int32_t acc = w[kWords - 1];
-#pragma unroll
-  for (int l = 0; l * 16 < kWords; ++l) acc ^= w[l * 16];
-  return acc;
-}
-
-__device__ __forceinline__ void warm_args(int32_t folded) { asm volatile("" : : "s"(folded)); }
-
 // ---- per-element arithmetic ------------------------------------------------
 
 struct FwdOut {

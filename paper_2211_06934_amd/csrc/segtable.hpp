@@ -75,6 +75,32 @@ struct TinyTable {
   int32_t orig[kTinyLeaves]{};   // the leaf's index in the caller's leaf-address arrays
 };
 
+// Element j of the concatenated leaves: its leaf's caller index and its index
+// in the leaf.  The scan is unrolled over the whole table (entries past the
+// last leaf start at INT32_MAX), so it reads the kernel arguments at fixed
+// offsets and takes no branch.  Each entry passes through an empty asm
+// statement so that it is selected as a value held in a scalar register:
+// otherwise the compiler selects its address instead and reads the chosen
+// entry with a per-lane load, one more memory round trip before the leaf
+// addresses can be loaded.
+__device__ __forceinline__ bool tiny_slot(const TinyTable& tt, int64_t j, int& orig, int64_t& i) {
+  if (j >= tt.total) return false;
+  const int32_t jj = (int32_t)j;
+  int o = tt.orig[0];
+  int32_t first = 0;
+#pragma unroll
+  for (int t = 1; t < kTinyLeaves; ++t) {
+    int32_t st = tt.start[t], ot = tt.orig[t];
+    asm volatile("" : "+s"(st), "+s"(ot));
+    const bool in = jj >= st;
+    o = in ? ot : o;
+    first = in ? st : first;
+  }
+  orig = o;
+  i = jj - first;
+  return true;
+}
+
 }  // namespace diffopt
 
 struct diffopt_segtable {
@@ -87,6 +113,7 @@ struct diffopt_segtable {
   int device = 0;
   int dense_orig = 1;               // no empty leaves: table index == leaf index
   int tiny = 0;                     // the leaves fit a TinyTable (held in `small`)
+  int contiguous = 0;               // every nonempty leaf's flat offset is the element count before it
   diffopt::TinyTable small;
   diffopt::SegEntry* d_seg = nullptr;       // [nact + 1]
   int64_t* d_tile_first = nullptr;  // [ntiles + 1]

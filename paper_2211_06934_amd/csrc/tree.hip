@@ -226,6 +226,30 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
   }
 }
 
+// Small trees whose flat layout is the plain concatenation of the leaves (a
+// TinyTable and no gaps): one element per lane, element j of the flat buffer
+// being element j of the concatenated leaves; the leaf comes from a scan of
+// the table in the kernel arguments, so a lane's only dependent loads are its
+// leaf's address and then the element.  The launch is bound by latency, not
+// bandwidth (1,761 elements: seven waves).
+constexpr int kTinyCB = 256;
+
+template <int E, bool PACK>
+__global__ __launch_bounds__(kTinyCB) void tree_copy_tiny(TinyTable tt, CopyBatch batch) {
+  warm_args(fold_lines(tt) ^ fold_lines(batch));
+  typedef typename ElemT<E>::T T;
+  const uint64_t* __restrict__ leaf_ptrs = batch.leaf_ptrs[blockIdx.y];
+  const uint64_t flat = batch.flat[blockIdx.y];
+  const int64_t j = (int64_t)blockIdx.x * kTinyCB + threadIdx.x;
+  int orig;
+  int64_t i;
+  if (!tiny_slot(tt, j, orig, i)) return;
+  const gptr<T> f = gaddr<T>(flat) + j;
+  const gptr<T> l = gaddr<T>(leaf_ptrs[orig]) + i;
+  if (PACK) *f = *l;
+  else *l = *f;
+}
+
 }  // namespace
 }  // namespace diffopt
 
@@ -290,6 +314,9 @@ extern "C" int diffopt_segtable_create(int64_t nseg, const int64_t* numel, const
   if (hipGetDevice(&t->device) != hipSuccess) t->device = -1;
   int64_t elems = 0;
   for (int64_t j = 0; j < nact; ++j) elems += host[(size_t)j].numel;
+  t->contiguous = 1;
+  for (int64_t j = 0, at = 0; j < nact; at += host[(size_t)j].numel, ++j)
+    if (host[(size_t)j].off != at) t->contiguous = 0;
   if (nact >= 1 && nact <= kTinyLeaves && elems <= kTinyElems) {
     t->tiny = 1;
     t->small.n = (int32_t)nact;
@@ -366,6 +393,26 @@ int tree_copy(const char* who, const diffopt_segtable* t, int64_t ntrees, const 
     for (int k = 0; k < nb; ++k) {
       batch.leaf_ptrs[k] = leaf_ptrs[k0 + k];
       batch.flat[k] = flat[k0 + k];
+    }
+    if (t->tiny && t->contiguous) {
+      const dim3 tgrid((unsigned)((t->small.total + kTinyCB - 1) / kTinyCB), (unsigned)nb);
+      switch (t->elem_bytes) {
+        case 1:
+          hipLaunchKernelGGL((tree_copy_tiny<1, PACK>), tgrid, dim3(kTinyCB), 0, st, t->small, batch);
+          break;
+        case 2:
+          hipLaunchKernelGGL((tree_copy_tiny<2, PACK>), tgrid, dim3(kTinyCB), 0, st, t->small, batch);
+          break;
+        case 4:
+          hipLaunchKernelGGL((tree_copy_tiny<4, PACK>), tgrid, dim3(kTinyCB), 0, st, t->small, batch);
+          break;
+        default:
+          hipLaunchKernelGGL((tree_copy_tiny<8, PACK>), tgrid, dim3(kTinyCB), 0, st, t->small, batch);
+          break;
+      }
+      int rc = launch_status(who);
+      if (rc) return rc;
+      continue;
     }
     dim3 grid((unsigned)t->ntiles, (unsigned)nb), block(kTB);
     switch (t->elem_bytes) {

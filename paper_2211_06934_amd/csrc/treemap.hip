@@ -606,32 +606,6 @@ static_assert(kTRS == 8, "launch_trbwd_c instantiates run lengths 1..8");
 // and one element's chain.
 constexpr int kTinyB = 256;
 
-// Element j of the concatenated leaves: its leaf's caller index and its index
-// in the leaf.  The scan is unrolled over the whole table (entries past the
-// last leaf start at INT32_MAX), so it reads the kernel arguments at fixed
-// offsets and takes no branch.  Each entry passes through an empty asm
-// statement so that it is selected as a value held in a scalar register:
-// otherwise the compiler selects its address instead and reads the chosen
-// entry with a per-lane load, one more memory round trip before the leaf
-// addresses can be loaded.
-__device__ __forceinline__ bool tiny_slot(const TinyTable& tt, int64_t j, int& orig, int64_t& i) {
-  if (j >= tt.total) return false;
-  const int32_t jj = (int32_t)j;
-  int o = tt.orig[0];
-  int32_t first = 0;
-#pragma unroll
-  for (int t = 1; t < kTinyLeaves; ++t) {
-    int32_t st = tt.start[t], ot = tt.orig[t];
-    asm volatile("" : "+s"(st), "+s"(ot));
-    const bool in = jj >= st;
-    o = in ? ot : o;
-    first = in ? st : first;
-  }
-  orig = o;
-  i = jj - first;
-  return true;
-}
-
 // Leaf addresses as global-space pointers (see gptr): every load below is then
 // a global_* instruction, counted by the vector-memory counter alone.
 __device__ __forceinline__ gptr<const float> leaf_in(const uint64_t* arr, int orig) {
@@ -832,6 +806,29 @@ __global__ __launch_bounds__(kUTB) void ew_tree_kernel(const SegEntry* __restric
   }
 }
 
+// Small trees (a TinyTable): one element per lane, the table in the kernel
+// arguments, every leaf address then every input loaded before the op, as in
+// the small-tree Adam kernels; the same op.apply per element.
+template <class Op>
+__global__ __launch_bounds__(kTinyB) void ew_tree_tiny(TinyTable tt, LeafArrays<Op::NIN + Op::NOUT> arr, Op op) {
+  warm_args(fold_lines(tt) ^ fold_lines(arr) ^ fold_lines(op));
+  int leaf;
+  int64_t i;
+  if (!tiny_slot(tt, (int64_t)blockIdx.x * kTinyB + threadIdx.x, leaf, i)) return;
+  gptr<const float> in[Op::NIN];
+  gptr<float> out[Op::NOUT];
+#pragma unroll
+  for (int a = 0; a < Op::NIN; ++a) in[a] = leaf_in(arr.a[a], leaf);
+#pragma unroll
+  for (int q = 0; q < Op::NOUT; ++q) out[q] = leaf_out(arr.a[Op::NIN + q], leaf);
+  float xi[Op::NIN], yo[Op::NOUT];
+#pragma unroll
+  for (int a = 0; a < Op::NIN; ++a) xi[a] = in[a][i];
+  op.apply(xi, yo);
+#pragma unroll
+  for (int q = 0; q < Op::NOUT; ++q) out[q][i] = yo[q];
+}
+
 // Runner of the leaf-direct kernel for the *_variant selectors: every
 // operand is a device array of leaf addresses.
 struct TreeRun {
@@ -843,8 +840,11 @@ struct TreeRun {
     LeafArrays<Op::NIN + Op::NOUT> arr{};
     for (int a = 0; a < Op::NIN; ++a) arr.a[a] = static_cast<const uint64_t*>(in[a]);
     for (int q = 0; q < Op::NOUT; ++q) arr.a[Op::NIN + q] = static_cast<const uint64_t*>(out[q]);
-    hipLaunchKernelGGL((ew_tree_kernel<Op>), dim3((unsigned)t->ntiles), dim3(kUTB), 0, st, t->d_seg,
-                       t->d_tile_first, t->ngroups, t->dense_orig, arr, op);
+    if (t->tiny)
+      hipLaunchKernelGGL((ew_tree_tiny<Op>), dim3(tiny_blocks(t)), dim3(kTinyB), 0, st, t->small, arr, op);
+    else
+      hipLaunchKernelGGL((ew_tree_kernel<Op>), dim3((unsigned)t->ntiles), dim3(kUTB), 0, st, t->d_seg,
+                         t->d_tile_first, t->ngroups, t->dense_orig, arr, op);
     return launch_status(who);
   }
 };

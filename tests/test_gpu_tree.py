@@ -3,7 +3,8 @@
 Bit-exact for every element size (1, 2, 4, 8 bytes), for dense and gapped
 layouts, for leaves whose addresses are out of phase with their flat offsets,
 for windows of many tiny leaves (the LDS window bound), empty leaves, special
-fp32 bit patterns, and the full 20,000-leaf workload.
+fp32 bit patterns, the full 20,000-leaf workload, and small tables on both
+sides of the limits of the one-element-per-lane copy.
 """
 import numpy as np
 import pytest
@@ -104,6 +105,38 @@ def test_explicit_offsets_with_gaps(eb):
         offsets[j] = pos
         pos += leaves[j].size + int(rng.integers(0, 7))
     _roundtrip(leaves, eb, "packed-views", seed=11, offsets=offsets)
+
+
+SMALL_TABLES = {  # at most 32 nonempty leaves and 2^16 elements, no gaps: one element per lane
+    "one-leaf": [1761],
+    "ragged-with-empties": [0, 3, 40, 1, 1600, 0, 40, 7, 1, 4096, 5, 2, 0],
+    "32-leaves": [(7 * k) % 23 + 1 for k in range(32)],
+    "33-leaves (tiled)": [(7 * k) % 23 + 1 for k in range(33)],
+    "2^16-elements": [1 << 15, 1, (1 << 15) - 4, 3],
+    "2^16+1-elements (tiled)": [1 << 15, 2, (1 << 15) - 4, 3],
+}
+
+
+@pytest.mark.parametrize("eb", [4, 1, 2, 8])
+@pytest.mark.parametrize("mode", ["separate", "packed-views"])
+@pytest.mark.parametrize("case", list(SMALL_TABLES))
+def test_small_tables_bit_exact(case, mode, eb):
+    ndt = DT[eb][0]
+    leaves = [random_bits(k, ndt, seed=31 * eb + i) for i, k in enumerate(SMALL_TABLES[case])]
+    _roundtrip(leaves, eb, mode, seed=eb + 5)
+
+
+@pytest.mark.parametrize("gap", [0, 3])
+def test_small_table_with_explicit_offsets(gap):
+    # offsets equal to the concatenation keep the one-element-per-lane copy;
+    # a gap makes the layout other than the concatenation (the tiled kernel)
+    numel = [40, 0, 1600, 7, 1]
+    leaves = [random_bits(k, np.float32, seed=70 + i) for i, k in enumerate(numel)]
+    offsets, pos = [], 0
+    for k in numel:
+        offsets.append(pos)
+        pos += k + (gap if k else 0)
+    _roundtrip(leaves, 4, "separate", seed=9, offsets=offsets)
 
 
 def test_special_values_survive():
