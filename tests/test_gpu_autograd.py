@@ -69,15 +69,16 @@ def test_adamfn_moment_cotangents_flow():
         assert np.all(np.abs(to(got) - r) <= BWD_RTOL * mg)
 
 
+@pytest.mark.parametrize("name", ["convnet32", "tiny_mlp"])  # tiled kernels; one element per lane
 @pytest.mark.parametrize("stored,K", [("all", 5), ("final", 5), ((5,), 10), ((7, 15), 17)])
-def test_unrolled_driver_in_hip_graph_replays(stored, K):
+def test_unrolled_driver_in_hip_graph_replays(stored, K, name):
     # "final": only the final moment state is stored and the backward
     # recomputes the trajectory; K = 10 with state 5 stored runs two recompute
     # launches; K = 17 with states 7 and 15 stored crosses the forward's 16-step launch
     # boundary on an unstored state (the running moments pass through the
     # final-state buffers)
     import paper_2211_06934_amd as P
-    w = WORKLOADS["convnet32"]()
+    w = WORKLOADS[name]()
     n = w.n
     inp = host_inputs(w)
     dev = "cuda"
@@ -153,13 +154,14 @@ def test_tree_flatten_in_hip_graph_replays():
         assert all(torch.equal(a, b) for a, b in zip(outs, leaves)), rep
 
 
-def test_leaf_direct_and_batched_entry_points_in_hip_graph_replay():
+@pytest.mark.parametrize("name", ["resnet18_k1", "tiny_mlp"])  # tiled kernels; the small-tree kernels
+def test_leaf_direct_and_batched_entry_points_in_hip_graph_replay(name):
     # every other launching entry point in one captured sequence: batched
     # pack/unpack, the leaf-direct K-step driver (trajectory recomputed),
     # leaf-direct SGD-momentum and RMSProp, and the ES perturb/estimate pair;
     # each replay must equal the eager run bit for bit
     import paper_2211_06934_amd as P
-    w = WORKLOADS["resnet18_k1"]()
+    w = WORKLOADS[name]()
     numel, n, K = w.numels, w.n, 3
     table = P.segtable_create(numel)
     gen = torch.Generator(device="cuda").manual_seed(5)
