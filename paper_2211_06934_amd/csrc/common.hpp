@@ -32,13 +32,19 @@ inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s);
 // of every line of an argument into a single value that an empty asm
 // statement consumes makes the kernel issue all of those loads at its start,
 // with one wait; the later reads of the same lines hit the cache.
+// The words are copied out with memcpy, the defined way to read an object's
+// bytes as another type.
 template <class T>
 __device__ __forceinline__ int32_t fold_lines(const T& x) {
   constexpr int kWords = (int)(sizeof(T) / 4);
-  const int32_t* w = reinterpret_cast<const int32_t*>(&x);
-  int32_t acc = w[kWords - 1];
+  const char* bytes = reinterpret_cast<const char*>(&x);
+  int32_t acc, w;
+  __builtin_memcpy(&acc, bytes + 4 * (kWords - 1), 4);
 #pragma unroll
-  for (int l = 0; l * 16 < kWords; ++l) acc ^= w[l * 16];
+  for (int l = 0; l * 16 < kWords; ++l) {
+    __builtin_memcpy(&w, bytes + 64 * l, 4);
+    acc ^= w;
+  }
   return acc;
 }
 
