@@ -114,6 +114,7 @@ SMALL_TABLES = {  # at most 32 nonempty leaves and 2^16 elements, no gaps: one e
     "33-leaves (tiled)": [(7 * k) % 23 + 1 for k in range(33)],
     "2^16-elements": [1 << 15, 1, (1 << 15) - 4, 3],
     "2^16+1-elements (tiled)": [1 << 15, 2, (1 << 15) - 4, 3],
+    "sparse-40-leaves": [0 if k % 4 else 3 * k + 1 for k in range(40)],  # 10 nonempty, indices up to 36
 }
 
 

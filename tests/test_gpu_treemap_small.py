@@ -30,6 +30,9 @@ SMALL = {
     "ragged": [0, 3, 40, 1, 1600, 0, 40, 7, 1, 4096, 5, 2, 0],
     "32-leaves": [(7 * k) % 23 + 1 for k in range(32)],
     "2^16-elements": [1 << 15, 1, (1 << 15) - 4, 3],
+    # 40 leaves of which 26 are empty: the small form, with caller leaf
+    # indices up to 39 (past the table's 32 slots)
+    "sparse": [0 if k % 4 else 3 * k + 1 for k in range(40)][:30] + [5, 0, 9, 0, 2, 0, 7, 0, 11, 4],
 }
 
 
