@@ -457,7 +457,9 @@ int diffopt_es_estimate(const float* noise, const float* weights,
  *            in [0, 1);
  *   z_ij   = sqrt(-2 ln u1) cos(2 pi u2) for even q, sqrt(-2 ln u1)
  *            sin(2 pi u2) for odd q (Box and Muller, 1958), computed in fp32
- *            (within a few fp32 ulp of the exact value times 1 + |z|).
+ *            with the hardware log2, square root, sine and cosine: within
+ *            3.5e-7 r of the exact value, r = sqrt(-2 ln u1) (measured over
+ *            every value the two uniforms can take).
  * The same seed gives the same z in both calls, and in any launch shape.
  *
  * es_perturb_gaussian: out as for diffopt_es_perturb ([N][n], or [2N][n]
