@@ -20,6 +20,9 @@
 #ifndef DIFFOPT_TREE_NT_LOADS
 #define DIFFOPT_TREE_NT_LOADS 0  // streaming loads of source vectors
 #endif
+#ifndef DIFFOPT_TREE_SHARE
+#define DIFFOPT_TREE_SHARE 1  // second source vector taken from the next lane
+#endif
 #ifndef DIFFOPT_TREE_NT_STORES
 #define DIFFOPT_TREE_NT_STORES 1  // streaming stores of full destination vectors
 #endif

@@ -10,12 +10,16 @@
 // alignment phase, so the G_j groups always cover the leaf; a group may be
 // partial (head, tail) or empty.  The rounding starts every leaf on a 128-byte
 // boundary of the group space, so for line-aligned destinations (leaves from an
-// allocator) tile boundaries never split a cache line between two tiles.  Each lane owns one group per step: full groups take one aligned
-// 128-bit store, fed by one or two aligned 128-bit loads of the source and a
-// funnel shift when source and destination phases differ (dense offsets put
-// ~3/4 of leaves out of phase with their flat range); partial groups copy
-// element by element.  Every byte is copied through integer registers, so NaN
-// payloads, signed zeros and subnormals survive.
+// allocator) tile boundaries never split a cache line between two tiles.
+// Each lane owns one group per step: full groups take one aligned 128-bit
+// store, fed by one or two aligned 128-bit source vectors and a funnel shift
+// when source and destination phases differ (dense offsets put ~3/4 of leaves
+// out of phase with their flat range); partial groups copy element by
+// element.  Consecutive lanes own consecutive groups, so within a leaf the
+// second source vector of one lane is the first of the next lane, which hands
+// it over through a cross-lane read instead of a second load.  Every byte is
+// copied through integer registers, so NaN payloads, signed zeros and
+// subnormals survive.
 //
 // Segment lookup.  Block b handles groups [b*TG, (b+1)*TG).  The host
 // precomputes tile_first[b], the leaf holding group b*TG; the leaves a tile
@@ -65,16 +69,17 @@ __device__ __forceinline__ uint32_t pick4(uint32_t a, uint32_t b, uint32_t c, ui
   return q == 0 ? a : (q == 1 ? b : (q == 2 ? c : d));
 }
 
-// The 16 bytes starting s bytes into the 32-byte window (w0, w1), 0 < s < 16.
+// The 16 bytes starting s bytes into the 32-byte window (w0, w1), 0 <= s < 16
+// (s = 0 gives w0, whatever w1 holds).
 template <int E>
 __device__ __forceinline__ u32x4 funnel(u32x4 w0, u32x4 w1, uint32_t s) {
   const uint32_t q = s >> 2;
-  if (E >= 4) {  // s is a multiple of 4: whole-dword selection, q in 1..3
+  if (E >= 4) {  // s is a multiple of 4: whole-dword selection
     u32x4 o;
-    o.x = q == 1 ? w0.y : (q == 2 ? w0.z : w0.w);
-    o.y = q == 1 ? w0.z : (q == 2 ? w0.w : w1.x);
-    o.z = q == 1 ? w0.w : (q == 2 ? w1.x : w1.y);
-    o.w = q == 1 ? w1.x : (q == 2 ? w1.y : w1.z);
+    o.x = pick4(w0.x, w0.y, w0.z, w0.w, q);
+    o.y = pick4(w0.y, w0.z, w0.w, w1.x, q);
+    o.z = pick4(w0.z, w0.w, w1.x, w1.y, q);
+    o.w = pick4(w0.w, w1.x, w1.y, w1.z, q);
     return o;
   } else {
     const uint32_t r = s & 3u;
@@ -162,14 +167,24 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
   // Phase 1 locates every group of this lane and issues all of its source
   // loads; phase 2 stores.  Sources never overlap destinations, so all loads
   // may go out before any store and each lane keeps kTreeU groups in flight.
+  // The first load of a group is issued by every lane, outside any branch:
+  // lanes without a full group read the first 16 bytes of the segment table
+  // (valid, aligned, cached) and discard them.  A load under a branch leaves
+  // its register undefined on the other path, and the join copied part of it
+  // into another register, which waited for the load to return and so held
+  // back the next group's search and loads.
   u32x4 w0[kTreeU], w1[kTreeU];
-  uint64_t dst[kTreeU], lo_b[kTreeU], hi_b[kTreeU], delta[kTreeU];
+  uint64_t dst[kTreeU], lo_b[kTreeU], hi_b[kTreeU], delta[kTreeU], src_v[kTreeU];
   uint32_t shift[kTreeU];
   int kind[kTreeU];  // 0: nothing, 1: full aligned vector, 2: partial (element copy)
+  bool own1[kTreeU];  // this lane loads its second source vector itself
 #pragma unroll
   for (int u = 0; u < kTreeU; ++u) {
     const int64_t gidx = b * kTileGroups + (int64_t)u * kTB + threadIdx.x;
     kind[u] = 0;
+    own1[u] = false;
+    shift[u] = 0;
+    src_v[u] = (uint64_t)seg;
     if (gidx < ngroups) {
       // largest t with s_goff[t] <= gidx; s_goff[0] <= gidx holds by construction
       int lo = 0, hi = W - 1;
@@ -194,31 +209,81 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
           kind[u] = 1;
           const uint64_t S = A + delta[u];
           shift[u] = (uint32_t)(S & 15u);
-          const gptr<const u32x4> L = gaddr<const u32x4>(S - shift[u]);
-#if DIFFOPT_TREE_NT_LOADS
-          w0[u] = __builtin_nontemporal_load(L);
-          if (shift[u] != 0) w1[u] = __builtin_nontemporal_load(L + 1);
+          src_v[u] = S - shift[u];
+#if DIFFOPT_TREE_SHARE
+          // Lane l+1 of the wave holds group gidx+1.  When that group is a
+          // full vector of the same leaf (same source-destination distance),
+          // its first source vector is this lane's second one, so this lane
+          // takes it from there instead of loading it again.
+          const bool next_full = (threadIdx.x & 63) != 63 && gidx + 1 < s_goff[lo + 1] && A + 32u <= dst0 + nb;
+          own1[u] = shift[u] != 0 && !next_full;
 #else
-          w0[u] = L[0];
-          if (shift[u] != 0) w1[u] = L[1];
+          own1[u] = shift[u] != 0;
 #endif
         } else {
           kind[u] = 2;
         }
       }
     }
+    const gptr<const u32x4> L = gaddr<const u32x4>(src_v[u]);
+    w1[u] = u32x4{0u, 0u, 0u, 0u};
+#if DIFFOPT_TREE_NT_LOADS
+    w0[u] = __builtin_nontemporal_load(L);
+#else
+    w0[u] = L[0];
+#endif
+    if (own1[u]) {
+      if (E >= 4) {
+        // Whole-dword shifts read only the first three words of the second
+        // vector.  Loading just those leaves the fourth register free, so it
+        // can be reused without waiting for the load.
+        const gptr<const uint32_t> L1 = gaddr<const uint32_t>(src_v[u] + 16u);
+        w1[u].x = L1[0];
+        w1[u].y = L1[1];
+        w1[u].z = L1[2];
+      } else {
+#if DIFFOPT_TREE_NT_LOADS
+        w1[u] = __builtin_nontemporal_load(L + 1);
+#else
+        w1[u] = L[1];
+#endif
+      }
+    }
   }
   typedef typename ElemT<E>::T T;
+#if DIFFOPT_TREE_SHARE
+  // Every lane of the wave takes part in the cross-lane reads (ds_bpermute
+  // from lane l+1; lane 63 wraps to lane 0 and never uses the value).
+  const int next_lane = (int)((((threadIdx.x & 63) + 1) & 63) << 2);
+#pragma unroll
+  for (int u = 0; u < kTreeU; ++u) {
+    u32x4 nv;
+    nv.x = (uint32_t)__builtin_amdgcn_ds_bpermute(next_lane, (int)w0[u].x);
+    nv.y = (uint32_t)__builtin_amdgcn_ds_bpermute(next_lane, (int)w0[u].y);
+    nv.z = (uint32_t)__builtin_amdgcn_ds_bpermute(next_lane, (int)w0[u].z);
+    nv.w = (uint32_t)__builtin_amdgcn_ds_bpermute(next_lane, (int)w0[u].w);
+    if (!own1[u]) w1[u] = nv;
+  }
+#endif
+  // Full groups first, partial groups after: the memory counter also counts
+  // stores and retires in order, so a load issued between stores would make
+  // the next full group's store wait for the earlier ones.
+  u32x4 out[kTreeU];
+#pragma unroll
+  for (int u = 0; u < kTreeU; ++u) out[u] = funnel<E>(w0[u], w1[u], shift[u]);
 #pragma unroll
   for (int u = 0; u < kTreeU; ++u) {
     if (kind[u] == 1) {
-      const u32x4 out = shift[u] != 0 ? funnel<E>(w0[u], w1[u], shift[u]) : w0[u];
 #if DIFFOPT_TREE_NT_STORES
-      __builtin_nontemporal_store(out, gaddr<u32x4>(dst[u]));
+      __builtin_nontemporal_store(out[u], gaddr<u32x4>(dst[u]));
 #else
-      *gaddr<u32x4>(dst[u]) = out;
+      *gaddr<u32x4>(dst[u]) = out[u];
 #endif
-    } else if (kind[u] == 2) {
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kTreeU; ++u) {
+    if (kind[u] == 2) {
       for (uint64_t x = lo_b[u]; x < hi_b[u]; x += E) {
         *gaddr<T>(x) = *gaddr<const T>(x + delta[u]);
       }
