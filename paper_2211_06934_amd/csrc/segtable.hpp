@@ -53,9 +53,21 @@ __device__ __forceinline__ gptr<T> gaddr(uint64_t addr) {
   return (gptr<T>)addr;
 }
 
+// Read-only memory that no kernel writes while it runs (the segment table and
+// the caller's leaf-address arrays), read at an address the same for the whole
+// workgroup: address space 4 lets the compiler use scalar loads, which issue
+// together and count on their own wait counter.
+template <typename T>
+using cptr = const __attribute__((address_space(4))) T*;
+
+template <typename T>
+__device__ __forceinline__ cptr<T> caddr(const void* addr) {
+  return (cptr<T>)(uint64_t)addr;
+}
+
 // One nonempty leaf, in table order.  The entry after the last nonempty leaf
 // is a sentinel whose goff is the total group count.
-struct SegEntry {
+struct SegEntry {  // four int64 fields in this order (read as such)
   int64_t goff;   // first group index
   int64_t off;    // flat element offset
   int64_t numel;  // elements

@@ -136,40 +136,24 @@ __device__ __forceinline__ int64_t tree_tile(int64_t b, int64_t ntiles) {
   return base + (l % 8) * R + l / 8;
 }
 
-template <int E, bool PACK>
-__global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restrict__ seg,
-                                                        const int64_t* __restrict__ tile_first, int64_t ngroups,
-                                                        CopyBatch batch, int dense_orig) {
-  const uint64_t* __restrict__ leaf_ptrs = batch.leaf_ptrs[blockIdx.y];
-  const uint64_t flat = batch.flat[blockIdx.y];
-  __shared__ int64_t s_goff[kWindowMax + 1];
-  __shared__ int64_t s_fbase[kWindowMax];  // flat byte address of the leaf's range
-  __shared__ int64_t s_bytes[kWindowMax];
-  __shared__ uint64_t s_leaf[kWindowMax];
+// The leaf holding a group, as the copy needs it: the leaf's first group and
+// the next leaf's, the flat byte address of its range, its byte size and its
+// address.
+struct LeafRef {
+  int64_t goff, goff_next;
+  uint64_t fbase, bytes, leaf;
+};
 
-  const int64_t b = tree_tile(blockIdx.x, gridDim.x);
-  const int64_t j0 = tile_first[b];
-  const int W = (int)(tile_first[b + 1] - j0 + 1);
-  for (int t = threadIdx.x; t <= W; t += kTB) {
-    // Without empty leaves the table index is the leaf index, so the leaf
-    // address is fetched alongside the table entry instead of after it.
-    const uint64_t lp = (dense_orig && t < W) ? leaf_ptrs[j0 + t] : 0;
-    const SegEntry e = seg[j0 + t];
-    s_goff[t] = e.goff;
-    if (t < W) {
-      s_fbase[t] = (int64_t)(flat + (uint64_t)(e.off * E));
-      s_bytes[t] = e.numel * E;
-      s_leaf[t] = dense_orig ? lp : leaf_ptrs[e.orig];
-    }
-  }
-  __syncthreads();
-
+// Copies the groups of tile b.  find(gidx) returns the leaf holding group
+// gidx; dummy is a valid, 16-byte aligned device address (see below).
+template <int E, bool PACK, class Find>
+__device__ __forceinline__ void copy_tile(const int64_t b, const int64_t ngroups, const uint64_t dummy, Find find) {
   // Phase 1 locates every group of this lane and issues all of its source
   // loads; phase 2 stores.  Sources never overlap destinations, so all loads
   // may go out before any store and each lane keeps kTreeU groups in flight.
   // The first load of a group is issued by every lane, outside any branch:
-  // lanes without a full group read the first 16 bytes of the segment table
-  // (valid, aligned, cached) and discard them.  A load under a branch leaves
+  // lanes without a full group read 16 bytes at dummy (the segment table:
+  // valid, aligned, cached) and discard them.  A load under a branch leaves
   // its register undefined on the other path, and the join copied part of it
   // into another register, which waited for the load to return and so held
   // back the next group's search and loads.
@@ -184,19 +168,13 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
     kind[u] = 0;
     own1[u] = false;
     shift[u] = 0;
-    src_v[u] = (uint64_t)seg;
+    src_v[u] = dummy;
     if (gidx < ngroups) {
-      // largest t with s_goff[t] <= gidx; s_goff[0] <= gidx holds by construction
-      int lo = 0, hi = W - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (s_goff[mid] <= gidx) lo = mid;
-        else hi = mid - 1;
-      }
-      const uint64_t k = (uint64_t)(gidx - s_goff[lo]);
-      const uint64_t fb = (uint64_t)s_fbase[lo];
-      const uint64_t lb = s_leaf[lo];
-      const uint64_t nb = (uint64_t)s_bytes[lo];
+      const LeafRef r = find(gidx);
+      const uint64_t k = (uint64_t)(gidx - r.goff);
+      const uint64_t fb = r.fbase;
+      const uint64_t lb = r.leaf;
+      const uint64_t nb = r.bytes;
       const uint64_t dst0 = PACK ? fb : lb;
       const uint64_t src0 = PACK ? lb : fb;
       const uint64_t A = (dst0 & ~uint64_t(15)) + 16u * k;
@@ -215,7 +193,7 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
           // full vector of the same leaf (same source-destination distance),
           // its first source vector is this lane's second one, so this lane
           // takes it from there instead of loading it again.
-          const bool next_full = (threadIdx.x & 63) != 63 && gidx + 1 < s_goff[lo + 1] && A + 32u <= dst0 + nb;
+          const bool next_full = (threadIdx.x & 63) != 63 && gidx + 1 < r.goff_next && A + 32u <= dst0 + nb;
           own1[u] = shift[u] != 0 && !next_full;
 #else
           own1[u] = shift[u] != 0;
@@ -289,6 +267,70 @@ __global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restri
       }
     }
   }
+}
+
+// A tile that lies in one leaf reads that leaf's entry into scalar registers
+// instead of staging a window in LDS: the entry, the next entry's first group
+// and, with DENSE (no empty leaves, so the table index is the leaf index), the
+// leaf's address are read together.  Extending this to windows of up to four
+// leaves (a lane picking its leaf by comparing its group with the leaf starts)
+// measured no faster on the 20,000-leaf tree, so wider windows keep the LDS
+// path.
+template <int E, bool PACK, bool DENSE>
+__device__ __forceinline__ void copy_tile_one_leaf(const SegEntry* seg, const uint64_t* leaf_ptrs, uint64_t flat,
+                                                   int64_t j0, int64_t b, int64_t ngroups) {
+  const cptr<int64_t> e = caddr<int64_t>(seg + j0);  // goff, off, numel, orig; then the next entry
+  int64_t goff = e[0], off = e[1], numel = e[2], goff_next = e[4];
+  uint64_t leaf = *caddr<uint64_t>(leaf_ptrs + (DENSE ? j0 : e[3]));
+  // The empty asm takes all five values at one point, so every read is issued
+  // before the single wait for them (left alone, the compiler issued the
+  // leaf-address read only after waiting for the entry).
+  asm volatile("" : "+s"(goff), "+s"(off), "+s"(numel), "+s"(goff_next), "+s"(leaf));
+  const LeafRef r{goff, goff_next, flat + (uint64_t)(off * E), (uint64_t)(numel * E), leaf};
+  copy_tile<E, PACK>(b, ngroups, (uint64_t)seg, [&](int64_t) { return r; });
+}
+
+template <int E, bool PACK, bool DENSE>
+__global__ __launch_bounds__(kTB) void tree_copy_kernel(const SegEntry* __restrict__ seg,
+                                                        const int64_t* __restrict__ tile_first, int64_t ngroups,
+                                                        CopyBatch batch) {
+  const uint64_t* __restrict__ leaf_ptrs = batch.leaf_ptrs[blockIdx.y];
+  const uint64_t flat = batch.flat[blockIdx.y];
+  __shared__ int64_t s_goff[kWindowMax + 1];
+  __shared__ int64_t s_fbase[kWindowMax];  // flat byte address of the leaf's range
+  __shared__ int64_t s_bytes[kWindowMax];
+  __shared__ uint64_t s_leaf[kWindowMax];
+
+  const int64_t b = tree_tile(blockIdx.x, gridDim.x);
+  const int64_t j0 = tile_first[b];
+  const int W = (int)(tile_first[b + 1] - j0 + 1);  // the same for every lane of the block
+  if (W == 1) {  // most tiles of large leaves
+    copy_tile_one_leaf<E, PACK, DENSE>(seg, leaf_ptrs, flat, j0, b, ngroups);
+    return;
+  }
+  for (int t = threadIdx.x; t <= W; t += kTB) {
+    // With DENSE the leaf address is fetched alongside the table entry
+    // instead of after it.
+    const uint64_t lp = (DENSE && t < W) ? leaf_ptrs[j0 + t] : 0;
+    const SegEntry e = seg[j0 + t];
+    s_goff[t] = e.goff;
+    if (t < W) {
+      s_fbase[t] = (int64_t)(flat + (uint64_t)(e.off * E));
+      s_bytes[t] = e.numel * E;
+      s_leaf[t] = DENSE ? lp : leaf_ptrs[e.orig];
+    }
+  }
+  __syncthreads();
+  copy_tile<E, PACK>(b, ngroups, (uint64_t)seg, [&](int64_t gidx) {
+    // largest t with s_goff[t] <= gidx; s_goff[0] <= gidx holds by construction
+    int lo = 0, hi = W - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_goff[mid] <= gidx) lo = mid;
+      else hi = mid - 1;
+    }
+    return LeafRef{s_goff[lo], s_goff[lo + 1], (uint64_t)s_fbase[lo], (uint64_t)s_bytes[lo], s_leaf[lo]};
+  });
 }
 
 // Small trees whose flat layout is the plain concatenation of the leaves (a
@@ -434,6 +476,16 @@ extern "C" int64_t diffopt_segtable_nseg(const diffopt_segtable* t) { return t ?
 
 namespace {
 
+template <int E, bool PACK>
+void launch_copy(dim3 grid, hipStream_t st, const diffopt_segtable* t, const CopyBatch& batch) {
+  if (t->dense_orig)
+    hipLaunchKernelGGL((tree_copy_kernel<E, PACK, true>), grid, dim3(kTB), 0, st, t->d_seg, t->d_tile_first,
+                       t->ngroups, batch);
+  else
+    hipLaunchKernelGGL((tree_copy_kernel<E, PACK, false>), grid, dim3(kTB), 0, st, t->d_seg, t->d_tile_first,
+                       t->ngroups, batch);
+}
+
 // ntrees copies of one structure: leaf_ptrs[t] is tree t's device array of
 // leaf addresses, flat[t] its flat buffer; up to kMaxBatch trees per launch.
 template <bool PACK>
@@ -479,23 +531,19 @@ int tree_copy(const char* who, const diffopt_segtable* t, int64_t ntrees, const 
       if (rc) return rc;
       continue;
     }
-    dim3 grid((unsigned)t->ntiles, (unsigned)nb), block(kTB);
+    const dim3 grid((unsigned)t->ntiles, (unsigned)nb);
     switch (t->elem_bytes) {
       case 1:
-        hipLaunchKernelGGL((tree_copy_kernel<1, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                           batch, t->dense_orig);
+        launch_copy<1, PACK>(grid, st, t, batch);
         break;
       case 2:
-        hipLaunchKernelGGL((tree_copy_kernel<2, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                           batch, t->dense_orig);
+        launch_copy<2, PACK>(grid, st, t, batch);
         break;
       case 4:
-        hipLaunchKernelGGL((tree_copy_kernel<4, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                           batch, t->dense_orig);
+        launch_copy<4, PACK>(grid, st, t, batch);
         break;
       default:
-        hipLaunchKernelGGL((tree_copy_kernel<8, PACK>), grid, block, 0, st, t->d_seg, t->d_tile_first, t->ngroups,
-                           batch, t->dense_orig);
+        launch_copy<8, PACK>(grid, st, t, batch);
         break;
     }
     int rc = launch_status(who);
