@@ -2,7 +2,8 @@
 
 Bit-exact for every element size (1, 2, 4, 8 bytes), for dense and gapped
 layouts, for leaves whose addresses are out of phase with their flat offsets,
-for windows of many tiny leaves (the LDS window bound), empty leaves, special
+for windows of many tiny leaves (the LDS window bound), leaves holding whole
+tiles (the single-entry path) with and without empty leaves, special
 fp32 bit patterns, the full 20,000-leaf workload, and small tables on both
 sides of the limits of the one-element-per-lane copy.
 """
@@ -105,6 +106,26 @@ def test_explicit_offsets_with_gaps(eb):
         offsets[j] = pos
         pos += leaves[j].size + int(rng.integers(0, 7))
     _roundtrip(leaves, eb, "packed-views", seed=11, offsets=offsets)
+
+
+@pytest.mark.parametrize("eb", [4, 1, 2, 8])
+@pytest.mark.parametrize("mode", ["separate", "packed-views"])
+@pytest.mark.parametrize("with_empty", [False, True])
+def test_large_leaves_bit_exact(eb, mode, with_empty):
+    # Leaves of 40 KiB and more hold whole tiles (8 KiB of destination each),
+    # which the kernel copies from a single table entry read into scalar
+    # registers; the tiny leaves between them give tiles that span several
+    # leaves. Empty leaves make the table index differ from the leaf index.
+    rng = np.random.default_rng(20 + eb)
+    ndt = DT[eb][0]
+    sizes = []
+    for k in range(9):
+        sizes.append((40 << 10) // eb + int(rng.integers(0, 3000)))
+        sizes.append(int(rng.integers(1, 40)))
+        if with_empty:
+            sizes.append(0)
+    leaves = [random_bits(k, ndt, seed=300 + 7 * eb + i) for i, k in enumerate(sizes)]
+    _roundtrip(leaves, eb, mode, seed=40 + eb)
 
 
 SMALL_TABLES = {  # at most 32 nonempty leaves and 2^16 elements, no gaps: one element per lane
