@@ -23,16 +23,18 @@
 //
 // Segment lookup.  Block b handles groups [b*TG, (b+1)*TG).  The host
 // precomputes tile_first[b], the leaf holding group b*TG; the leaves a tile
-// touches are the window tile_first[b] .. tile_first[b+1].  The block stages
-// that window (group offsets, flat offsets, byte sizes, leaf addresses) in LDS
+// touches are the window tile_first[b] .. tile_first[b+1].  A window of one
+// leaf is read straight into scalar registers.  Otherwise the block stages
+// the window (group offsets, flat offsets, byte sizes, leaf addresses) in LDS
 // once, then every lane binary-searches the LDS window for its group.  Since
 // every nonempty leaf owns >= 8 groups, a window never exceeds TG/8 + 1
 // leaves, which bounds the LDS footprint.
 //
-// Page safety of the two source loads: a full group's 16 source bytes are all
-// valid leaf bytes, the first aligned source vector contains the first of them
-// and the second contains the last, and an aligned 16-byte vector never spans
-// two pages, so neither load touches a page the copy does not already use.
+// Page safety of the two source vectors: a full group's 16 source bytes are
+// all valid leaf bytes, the first aligned source vector contains the first of
+// them and the second contains the last, and an aligned 16-byte vector never
+// spans two pages, so no load touches a page the copy does not already use
+// (a lane that takes its second vector from the next lane loads nothing more).
 #include <algorithm>
 #include <cstdlib>
 #include <cstring>
