@@ -32,10 +32,11 @@ namespace diffopt {
 constexpr int kTreeU = DIFFOPT_TREE_U;
 constexpr int kTB = DIFFOPT_TREE_BLOCK;
 constexpr int64_t kTileGroups = (int64_t)kTB * kTreeU;
-// Every nonempty leaf owns a multiple of kLeafGroupAlign groups, so leaves
-// start on 8-group (128-byte) boundaries of the group space: tile boundaries
-// then fall on line boundaries of 128-byte aligned leaves, and a tile touches at
-// most kTileGroups / 8 + 1 leaves.
+// Every nonempty leaf owns a multiple of kLeafGroupAlign groups (at least 16),
+// so leaves start on 8-group (128-byte) boundaries of the group space: tile
+// boundaries then fall on line boundaries of the copy's destination and of
+// 128-byte aligned leaves, and a tile touches at most kTileGroups / 8 + 1
+// leaves.
 constexpr int64_t kLeafGroupAlign = 8;
 constexpr int kWindowMax = (int)(kTileGroups / kLeafGroupAlign + 2);
 

@@ -3,14 +3,16 @@
 //
 // Work decomposition.  Every copy writes whole, naturally aligned 16-byte
 // vectors of its DESTINATION (the flat buffer for flatten, the leaves for
-// unflatten).  Nonempty leaf j owns G_j = ceil(bytes_j / 16) + 1 consecutive
+// unflatten).  Nonempty leaf j owns G_j = ceil(bytes_j / 16) + 8 consecutive
 // "groups" of a global group index space, rounded up to a multiple of 8; group
 // k of leaf j is the aligned 16-byte destination vector number k counted from
-// the vector that holds the leaf's first destination byte.  The +1 covers any
-// alignment phase, so the G_j groups always cover the leaf; a group may be
-// partial (head, tail) or empty.  The rounding starts every leaf on a 128-byte
-// boundary of the group space, so for line-aligned destinations (leaves from an
-// allocator) tile boundaries never split a cache line between two tiles.
+// the 128-byte line that holds the leaf's first destination byte.  The +8
+// covers any phase within that line, so the G_j groups always cover the leaf;
+// a group may be partial (head, tail) or empty.  Leaves start on multiples of
+// 8 groups and tiles hold multiples of 8 groups, so every tile boundary falls
+// on a line boundary of the destination, for pack (the flat buffer, whatever
+// the leaves' offsets) as for unpack: no line is written in parts by two
+// tiles.
 // Each lane owns one group per step: full groups take one aligned 128-bit
 // store, fed by one or two aligned 128-bit source vectors and a funnel shift
 // when source and destination phases differ (dense offsets put ~3/4 of leaves
@@ -179,7 +181,7 @@ __device__ __forceinline__ void copy_tile(const int64_t b, const int64_t ngroups
       const uint64_t nb = r.bytes;
       const uint64_t dst0 = PACK ? fb : lb;
       const uint64_t src0 = PACK ? lb : fb;
-      const uint64_t A = (dst0 & ~uint64_t(15)) + 16u * k;
+      const uint64_t A = (dst0 & ~uint64_t(127)) + 16u * k;  // groups count from dst0's line
       lo_b[u] = A > dst0 ? A : dst0;
       hi_b[u] = (A + 16u) < (dst0 + nb) ? (A + 16u) : (dst0 + nb);
       delta[u] = src0 - dst0;  // modular; the source byte of x is x + delta
@@ -395,7 +397,7 @@ extern "C" int diffopt_segtable_create(int64_t nseg, const int64_t* numel, const
     run = off + k;
     if (k == 0) continue;
     total = std::max(total, off + k);
-    const int64_t need = (k * elem_bytes + 15) / 16 + 1;  // +1 absorbs any destination phase
+    const int64_t need = (k * elem_bytes + 15) / 16 + 8;  // +8 absorbs any phase within the first line
     const int64_t groups = (need + kLeafGroupAlign - 1) / kLeafGroupAlign * kLeafGroupAlign;
     host.push_back(SegEntry{goff, off, k, j});
     ranges.emplace_back(off, off + k);
