@@ -363,22 +363,33 @@ __global__ __launch_bounds__(kEB) void es_perturb_gauss(const float* theta, int6
 // in 64-chunk spans that start on a line, chunk c = 64 q + lane - d: only the
 // two lines at the workgroup's ends are shared with a neighbour (1.18 ms).
 // Measured on MI355X (n = 11,689,512, N = 64 antithetic, two rounds): 8 waves
-// per workgroup 1.18 ms, 4 waves 1.20, 2 waves 1.24; 4, 8 or 16 samples per
-// lane within 1%.
+// per workgroup 1.18 ms, 4 waves 1.20, 2 waves 1.24 (with the sample groups
+// outermost in the grid; the order is now chunk-major, below).
 #ifndef DIFFOPT_ES_LINE_WAVES
 #define DIFFOPT_ES_LINE_WAVES 8
 #endif
 constexpr int kLW = DIFFOPT_ES_LINE_WAVES;  // waves (segments) per workgroup
+// Samples per workgroup.  The grid is one-dimensional with the sample groups
+// of one parameter chunk consecutive, so the dispatcher runs them side by side
+// and they share the chunk's theta through the cache.  Measured (n =
+// 11,689,512, N = 64, six paired rounds): chunk-major order with 8, 4 or 2
+// samples per workgroup 1.138, 1.129, 1.137 ms, against 1.176 ms for the
+// sample groups outermost (8 per workgroup; 16, 32, 64: 1.185, 1.203, 1.257).
+#ifndef DIFFOPT_ES_LINE_ROWS
+#define DIFFOPT_ES_LINE_ROWS 4
+#endif
+constexpr int kLRows = DIFFOPT_ES_LINE_ROWS;
 constexpr int kLB = 64 * kLW;
 constexpr int kRowChunks = kLW * 128;  // 16-byte chunks of one row per workgroup
 
 __global__ __launch_bounds__(kLB) void es_perturb_gauss_lines(const float* theta, int64_t N, int64_t n,
                                                                uint64_t seed, float sigma, int antithetic,
-                                                               float* out) {
+                                                               uint32_t groups, float* out) {
   __shared__ f32x4 rows[2][kRowChunks];  // the plus and minus rows of one sample
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t b = (int64_t)blockIdx.x * kLB + threadIdx.x;
-  const int64_t first = (int64_t)blockIdx.x * (kRowChunks * 4);  // the workgroup's first parameter
+  const uint32_t chunk = blockIdx.x / groups, group = blockIdx.x - chunk * groups;
+  const int64_t b = (int64_t)chunk * kLB + threadIdx.x;
+  const int64_t first = (int64_t)chunk * (kRowChunks * 4);  // the workgroup's first parameter
   const int64_t left = (n - first) >> 2;                          // n % 4 == 0 here
   const int nchunks = left < kRowChunks ? (int)left : kRowChunks;
   bool on[2];
@@ -390,8 +401,8 @@ __global__ __launch_bounds__(kLB) void es_perturb_gauss_lines(const float* theta
 #pragma unroll
     for (int e = 0; e < 4; ++e) t[4 * h + e] = a[e];
   }
-  const int64_t i0 = (int64_t)blockIdx.y * kGRows;
-  const int64_t i1 = i0 + kGRows < N ? i0 + kGRows : N;
+  const int64_t i0 = (int64_t)group * kLRows;
+  const int64_t i1 = i0 + kLRows < N ? i0 + kLRows : N;
   const int nrows = antithetic ? 2 : 1;
   for (int64_t i = i0; i < i1; ++i) {
     if (on[0]) {  // a lane past the end computes nothing but still meets both barriers
@@ -580,10 +591,12 @@ extern "C" int diffopt_es_perturb_gaussian(const float* params, int64_t n, int64
   if (bx > 0x7fffffff) return fail(DIFFOPT_EINVAL, "%s: n too large", who);
   hipStream_t st = as_stream(stream);
   const dim3 grid((unsigned)bx, (unsigned)gy);
-  if (n % 4 == 0 && al16(params) && al16(out))
-    hipLaunchKernelGGL(es_perturb_gauss_lines, dim3((unsigned)((blocks + kLB - 1) / kLB), (unsigned)gy), dim3(kLB),
-                       0, st, params, num_samples, n, seed, (float)sigma, antithetic ? 1 : 0, out);
-  else
+  if (n % 4 == 0 && al16(params) && al16(out)) {
+    const int64_t chunks = (blocks + kLB - 1) / kLB, lgroups = (num_samples + kLRows - 1) / kLRows;
+    if (chunks * lgroups > 0x7fffffff) return fail(DIFFOPT_EINVAL, "%s: n x num_samples too large", who);
+    hipLaunchKernelGGL(es_perturb_gauss_lines, dim3((unsigned)(chunks * lgroups)), dim3(kLB), 0, st, params,
+                       num_samples, n, seed, (float)sigma, antithetic ? 1 : 0, (uint32_t)lgroups, out);
+  } else
     hipLaunchKernelGGL(es_perturb_gauss<false>, grid, dim3(kEB), 0, st, params, num_samples, n, seed, (float)sigma,
                        antithetic ? 1 : 0, out);
   return launch_status(who);
