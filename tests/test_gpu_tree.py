@@ -111,11 +111,14 @@ def test_explicit_offsets_with_gaps(eb):
 @pytest.mark.parametrize("eb", [4, 1, 2, 8])
 @pytest.mark.parametrize("mode", ["separate", "packed-views"])
 @pytest.mark.parametrize("with_empty", [False, True])
-def test_large_leaves_bit_exact(eb, mode, with_empty):
+@pytest.mark.parametrize("layout", ["dense", "permuted-gaps"])
+def test_large_leaves_bit_exact(eb, mode, with_empty, layout):
     # Leaves of 40 KiB and more hold whole tiles (8 KiB of destination each),
     # which the kernel copies from a single table entry read into scalar
     # registers; the tiny leaves between them give tiles that span several
-    # leaves. Empty leaves make the table index differ from the leaf index.
+    # leaves. Empty leaves make the table index differ from the leaf index;
+    # explicit offsets in another order than the table's, with gaps, put the
+    # leaves at arbitrary phases of the flat buffer's lines.
     rng = np.random.default_rng(20 + eb)
     ndt = DT[eb][0]
     sizes = []
@@ -125,7 +128,15 @@ def test_large_leaves_bit_exact(eb, mode, with_empty):
         if with_empty:
             sizes.append(0)
     leaves = [random_bits(k, ndt, seed=300 + 7 * eb + i) for i, k in enumerate(sizes)]
-    _roundtrip(leaves, eb, mode, seed=40 + eb)
+    offsets = None
+    if layout == "permuted-gaps":
+        order = rng.permutation(len(leaves))
+        offsets = [0] * len(leaves)
+        pos = int(rng.integers(0, 5))
+        for j in order:
+            offsets[j] = pos
+            pos += leaves[j].size + int(rng.integers(0, 7))
+    _roundtrip(leaves, eb, mode, seed=40 + eb, offsets=offsets)
 
 
 SMALL_TABLES = {  # at most 32 nonempty leaves and 2^16 elements, no gaps: one element per lane
